@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark: one MoE layer's dispatch + combine hot path on one MI355X.
+
+A step is one pass of the whole hot path over one synthetic batch:
+  epl_layout (routing layout) -> epl_dispatch (row scatter) -> epl_combine (gather-reduce),
+with identity experts in between (combine reads the receive buffer). All inputs are resident
+in HBM before timing starts.
+
+Default workload: EP=64 decode. 64 virtual ranks, 256 experts (4 per rank), top-8, 128
+tokens per rank (8192 tokens), hidden 7168 bf16, uniform routing without replacement, softmax
+gate weights.
+
+Output: one JSON line. It carries:
+* effective HBM GB/s, computed from the algorithmic bytes per layer;
+* µs per layer and per call;
+* the roofline entry of the dominant kernel, timed with HIP events on its own stream;
+* the CPU oracle timed on the host as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "dispatch+combine µs/MoE layer and effective HBM GB/s (% of peak), EP=64 decode"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2607_06202_amd", "csrc")
+
+
+def algorithmic_bytes(T, k, H, R, E, P, payload):
+    """Bytes the method itself must move (each token row read once, each pair row written once
+    by dispatch and read once by combine, the routing tables read and the metadata written)."""
+    NB = H // 128
+    b = 1 if payload == "fp8" else 2
+    dispatch = T * H * 2 + T * k * 4 + P * H * b + (P * NB * 4 if payload == "fp8" else 0)
+    combine = P * H * 2 + 2 * T * k * 4 + T * H * 2
+    layout = T * k * 4 + 4 * (R * E + R * R + (E + 1) + (R + 1) + E * R + T + 2 * T * k + 2 * P + 1)
+    return {"layout": layout, "dispatch": dispatch, "combine": combine,
+            "total": layout + dispatch + combine}
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were taken on the
+    current kernel sources; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    ent = rec.get("kernels", {}).get("%s@%s" % (kernel, workload))
+    if not ent or ent.get("source_hash") != source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(w, idx, x, gw, budget_s):
+    """The oracle (plain single-threaded C), timed on this host's CPU on the same inputs."""
+    import oracle
+
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        L = oracle.layout(w.R, w.E, w.k, w.Tr, idx)
+        if w.payload == "fp8":
+            recv, _ = oracle.dispatch_fp8(x, L.pair_row, L.P)
+            y = None
+        else:
+            recv = oracle.dispatch_bf16(x, L.pair_row, L.P)
+            y = recv
+        if y is not None:
+            oracle.combine(y, gw, L.pair_row)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 50:
+            break
+    return el / reps, reps, L.P
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="decode_ep64")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cold-steps", type=int, default=30, help="extra cold-cache steps (0 to skip)")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time (0 to skip)")
+    ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the single-GPU hot path only: every expert-parallel rank is a virtual rank "
+              "in one GPU's HBM; --gpus %d (WORLD_SIZE %d) is not supported" % (args.gpus, world),
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_06202_amd import epl
+    from paper_2607_06202_amd import workloads as W
+
+    if not os.path.exists(epl.LIB_PATH):
+        from paper_2607_06202_amd import _build
+        _build.build()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+
+    if args.calibrate_copy:
+        n = 1 << 30
+        a = torch.empty(n, dtype=torch.uint8, device=dev).random_(0, 255)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            b.copy_(a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "ms": ms,
+                          "GBps": 2 * n / ms / 1e6}))
+        return
+
+    w = W.WORKLOADS[args.workload]
+    idx = W.routing(w, args.seed)
+    x = W.tokens_bf16(w, args.seed)
+    gw = W.gate_weights(w, args.seed)
+    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)
+
+    idx_d = torch.from_numpy(idx).to(dev)
+    x_d = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
+    w_d = torch.from_numpy(gw).to(dev)
+    L = epl.alloc_layout(cfg, dev)
+    recv, recv_scale = epl.alloc_recv(cfg, dev)
+    out = torch.empty(w.T, w.H, dtype=torch.bfloat16, device=dev)
+    if w.payload == "fp8":
+        # combine reads bf16 expert outputs; identity experts would dequantise -- here a bf16
+        # buffer of the same shape stands in for them (not timed)
+        y = torch.zeros(epl.recv_rows_cap(cfg), w.H, dtype=torch.bfloat16, device=dev)
+    else:
+        y = recv
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        epl.layout(cfg, idx_d, out=L)
+        if ev is not None:
+            ev[1].record(stream)
+        epl.dispatch(cfg, x_d, L, recv, recv_scale)
+        if ev is not None:
+            ev[2].record(stream)
+        epl.combine(cfg, y, w_d, L, out)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    P = int(L.expert_off[-1].item())
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])] for e in evs])
+    us_layout, us_dispatch, us_combine = (per.mean(axis=0) * 1e3).tolist()
+    us_layer_events = float(per.sum(axis=1).mean() * 1e3)
+
+    nbytes = algorithmic_bytes(w.T, w.k, w.H, w.R, w.E, P, w.payload)
+    value = nbytes["total"] / (ms_per_step * 1e-3) / 1e9
+
+    dom = "dispatch" if us_dispatch >= us_combine else "combine"
+    dom_us = us_dispatch if dom == "dispatch" else us_combine
+    achieved = nbytes[dom] / (dom_us * 1e-6) / 1e9
+    kname = {"dispatch": "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
+             "combine": "combine_kernel"}[dom]
+    roofline = {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": load_traffic(kname, w.name), "algorithmic_bytes": nbytes[dom],
+                "avg_launch_us": round(dom_us, 2)}
+
+    cold = None
+    if args.cold_steps > 0:
+        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB, evicts L2 and MALL
+        cper = []
+        for _ in range(args.cold_steps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            flush.zero_()
+            ev[0].record(stream)
+            epl.layout(cfg, idx_d, out=L)
+            ev[1].record(stream)
+            flush.zero_()
+            ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev2[0].record(stream)
+            epl.dispatch(cfg, x_d, L, recv, recv_scale)
+            ev2[1].record(stream)
+            flush.zero_()
+            ev3 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev3[0].record(stream)
+            epl.combine(cfg, y, w_d, L, out)
+            ev3[1].record(stream)
+            torch.cuda.synchronize()
+            cper.append([ev[0].elapsed_time(ev[1]), ev2[0].elapsed_time(ev2[1]), ev3[0].elapsed_time(ev3[1])])
+        c = np.median(np.array(cper), axis=0) * 1e3
+        cold = {"us_layout": round(float(c[0]), 2), "us_dispatch": round(float(c[1]), 2),
+                "us_combine": round(float(c[2]), 2), "us_per_layer": round(float(c.sum()), 2),
+                "GBps": round(nbytes["total"] / (c.sum() * 1e-6) / 1e9, 1),
+                "note": "median over steps; 1 GiB write before each call, outside the timed events"}
+        del flush
+
+    cpu = None
+    if args.cpu_budget > 0:
+        sec, reps, P_ref = cpu_baseline(w, idx, x, gw, args.cpu_budget)
+        assert P_ref == P
+        cpu = {"value": round(nbytes["total"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "us_per_layer": round(sec * 1e6, 1),
+               "sample": "%d full %s layer(s) (layout+dispatch+combine) on the same inputs, single thread" % (
+                   reps, w.name)}
+
+    rec = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.payload, "data": "synthetic",
+        "config": {"workload": w.name, "ranks": w.R, "experts": w.E, "topk": w.k, "tokens_per_rank": w.T // w.R,
+                   "hidden": w.H, "payload": w.payload, "routing": w.routing, "pairs": P, "seed": args.seed},
+        "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_events": round(us_layer_events, 2),
+        "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2), "us_combine": round(us_combine, 2),
+        "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
+        "roofline": roofline, "cold": cold, "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()

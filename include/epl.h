@@ -1,0 +1,161 @@
+/*
+ * epl.h -- MoE expert-parallel token dispatch and combine on one MI355X (gfx950), C ABI.
+ *
+ * The operation (UBEP paper, Background "Deploying MoE on CM384" and the Overview):
+ *   - Dispatch routes every (token, chosen expert) pair to the rank hosting that expert.
+ *   - The receive space is split by (source rank, expert) and sized from per-expert token
+ *     counts. The counts are turned into prefix-sum offsets ("CalCumSum", Kernel Decomposition)
+ *     so that each expert's tokens end up contiguous ("Token-Reordering").
+ *   - Combine gathers the expert outputs back into token order.
+ *   - Senders write straight into pre-partitioned receive space (Implementation, global
+ *     load/store).
+ * Here all R expert-parallel ranks are virtual ranks in one GPU's HBM:
+ *   - rank s sends tokens [s*Tr, (s+1)*Tr) of x;
+ *   - rank d receives rows [rank_off[d], rank_off[d+1]) of the one packed receive buffer.
+ *
+ * Notation:
+ *   R = num_ranks, E = num_experts (E % R == 0), El = E/R experts per rank;
+ *   rank d owns experts [d*El, (d+1)*El);
+ *   k = topk, H = hidden, Tr = tokens_per_rank, T = R*Tr;
+ *   pair p = g*k + j is (token g, choice j);
+ *   it is valid iff 0 <= topk_idx[p] < E, and P = number of valid pairs.
+ *
+ * Receive layout:
+ *   - The valid pairs, stably sorted by expert id, take packed rows 0..P-1.
+ *   - So rows run in (destination rank, expert, source rank, token, j) order, with no gaps.
+ *
+ * Conventions:
+ *   - Every pointer argument is a DEVICE pointer unless stated. The caller allocates and owns
+ *     every buffer, including the workspace. The library allocates nothing and keeps no state
+ *     between calls.
+ *   - Each call checks its arguments on the host, enqueues kernels on `stream` (a hipStream_t;
+ *     NULL means the null stream) and returns without synchronising. Outputs are valid once the
+ *     stream reaches that point.
+ *   - Argument errors are reported BEFORE anything is enqueued.
+ *   - Data-dependent anomalies are not errors: an expert id outside [0, E) is skipped and
+ *     counted in *num_invalid.
+ *   - Payload pointers (x, recv, y, out) must be 16-byte aligned. Index, count, weight and
+ *     scale pointers must be 4-byte aligned.
+ */
+#ifndef EPL_H
+#define EPL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EPL_MAX_EXPERTS 1024 /* E (and therefore R) upper bound                        */
+#define EPL_MAX_TOPK 32      /* k upper bound                                            */
+
+typedef enum {
+  EPL_OK = 0,
+  EPL_ERR_INVALID_ARG = 1, /* bad config value, NULL where a buffer is required            */
+  EPL_ERR_ALIGN = 2,       /* a pointer violates the alignment rule above                 */
+  EPL_ERR_CAPACITY = 3,    /* recv_rows_cap < T*k                                          */
+  EPL_ERR_WORKSPACE = 4,   /* workspace smaller than epl_workspace_bytes()                 */
+  EPL_ERR_UNSUPPORTED = 5, /* fp8 payload with H % 128 != 0, unknown payload kind          */
+  EPL_ERR_DEVICE = 6       /* the HIP runtime refused a launch                             */
+} epl_status;
+
+typedef enum { EPL_PAYLOAD_BF16 = 0, EPL_PAYLOAD_FP8_E4M3 = 1 } epl_payload;
+
+typedef struct {
+  int32_t num_ranks;       /* R >= 1                                                     */
+  int32_t num_experts;     /* E, R <= E <= EPL_MAX_EXPERTS, E % R == 0                   */
+  int32_t topk;            /* k, 1..EPL_MAX_TOPK                                         */
+  int32_t hidden;          /* H >= 8, H % 8 == 0 (bf16); H % 128 == 0 for fp8 dispatch   */
+  int32_t tokens_per_rank; /* Tr >= 0; T*k < 2^31                                        */
+  int32_t payload;         /* epl_payload: dispatch output format                        */
+} epl_config;
+
+/* Layout outputs: int32 device arrays, caller-allocated, all required (non-NULL).
+ * send_cnt  [R*E]  send_cnt[s*E+e]: valid pairs of source rank s routed to expert e (the
+ *                  per-expert token counts each source reports).
+ * rank_cnt  [R*R]  rank_cnt[s*R+r]: tokens of source rank s with at least one valid pair on
+ *                  rank r (tokens after per-token destination-rank dedup).
+ * expert_off[E+1]  exclusive prefix sum of per-expert receive counts (CalCumSum); P = [E].
+ * rank_off  [R+1]  rank_off[d] = expert_off[d*El]: rank d's rows in the packed buffer.
+ * seg_off   [E*R]  seg_off[e*R+s] = expert_off[e] + sum_{s'<s} send_cnt[s'*E+e]: the
+ *                  (source rank, expert) segment of the receive space.
+ * tok_nranks[T]    number of distinct destination ranks of token g.
+ * pair_row  [T*k]  packed receive row of pair p, or -1 if p is invalid.
+ * pair_rslot[T*k]  for valid p: index of token g among the tokens of its source rank bound for
+ *                  rank(topk_idx[p]), in token order (pairs of one token on one rank share
+ *                  it); -1 if invalid.
+ * recv_src  [T*k]  recv_src[row] = token of packed row `row`, rows 0..P-1; rows >= P untouched.
+ * recv_j    [T*k]  recv_j[row] = choice index j of packed row `row`; rows >= P untouched.
+ * num_invalid[1]   number of pairs whose expert id lies outside [0, E).                   */
+typedef struct {
+  int32_t *send_cnt;
+  int32_t *rank_cnt;
+  int32_t *expert_off;
+  int32_t *rank_off;
+  int32_t *seg_off;
+  int32_t *tok_nranks;
+  int32_t *pair_row;
+  int32_t *pair_rslot;
+  int32_t *recv_src;
+  int32_t *recv_j;
+  int32_t *num_invalid;
+} epl_layout_buffers;
+
+/* Bytes of device workspace epl_layout needs for `cfg` (host-only, no HIP calls). Returns 0
+ * if cfg is invalid. The workspace holds per-chunk histograms and needs no initialisation. */
+size_t epl_workspace_bytes(const epl_config *cfg);
+
+/* Routing layout: per-(source rank, expert) histogram, CalCumSum prefix scans, stable slot
+ * assignment and per-token destination-rank dedup (Background phases 3 and 5; Kernel
+ * Decomposition: TokenCnt and CalCumSum).
+ *   topk_idx  [T*k] int32, row-major [T][k], read-only.
+ *   L         output buffers above, fully overwritten (recv_src/recv_j: rows 0..P-1 only).
+ *   workspace device scratch of at least epl_workspace_bytes(cfg), 4-byte aligned; its contents
+ *             on entry are ignored.
+ * Deterministic: identical inputs give bit-identical outputs; no atomic decides an order.    */
+epl_status epl_layout(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/* Dispatch: write every valid pair's token row into its packed receive row (the paper's
+ * Token-Sending into pre-partitioned receive space, with Token-Reordering fused because all
+ * offsets are known before any row is written).
+ *   x          [T*H] bf16 bit patterns, row-major, read-only; must not alias recv.
+ *   L          a layout produced by epl_layout for the same cfg (pair_row is read).
+ *   recv       [recv_rows_cap * H] elements: bf16 (2 bytes) for EPL_PAYLOAD_BF16, or E4M3
+ *              bytes for EPL_PAYLOAD_FP8_E4M3. Rows 0..P-1 are written, rows >= P untouched.
+ *   recv_scale fp8 only: [recv_rows_cap * H/128] fp32. Scale b of a row covers columns
+ *              [128b, 128b+128): s = max|x| / 448 over the block (IEEE fp32 division),
+ *              q = E4M3(x / s) rounded to nearest-even with saturation to +-448, sign kept on
+ *              zero, and s = 0, q = 0 for an all-zero block. Ignored (may be NULL) for bf16.
+ *   recv_rows_cap  rows available in recv; must be >= T*k (T*k bounds P without a sync).  */
+epl_status epl_dispatch(const epl_config *cfg, const void *x, const epl_layout_buffers *L, void *recv,
+                        float *recv_scale, int64_t recv_rows_cap, void *stream);
+
+/* Combine: gate-weighted gather-reduce of expert output rows back into token order (the
+ * paper's combine: gather expert outputs, restore token order).
+ *   y       [>= P rows][H] bf16 expert outputs, row r holds the expert result for packed row r.
+ *   topk_w  [T*k] fp32 gate weights, applied as given (no renormalisation).
+ *   out     [T*H] bf16. For every token g and column c:
+ *             acc = +0.0f; for j = 0..k-1 with pair_row[g*k+j] >= 0:
+ *                 acc = fmaf(topk_w[g*k+j], float(y[pair_row[g*k+j]][c]), acc);
+ *             out[g][c] = bf16 round-to-nearest-even(acc).
+ *           A token with no valid pair gets +0. out may alias x. out must not alias y.       */
+epl_status epl_combine(const epl_config *cfg, const void *y, const float *topk_w, const epl_layout_buffers *L,
+                       void *out, void *stream);
+
+/* Diagnostics: apply the exact device number conversions used by epl_dispatch (fp32 ->
+ * saturating E4M3) and epl_combine (fp32 -> bf16 RNE) to n values, for exhaustive checks.
+ * in [n] fp32, out [n] bytes / bf16 bit patterns, 4-byte aligned; n >= 0.                   */
+epl_status epl_debug_f32_to_e4m3(const float *in, uint8_t *out, int64_t n, void *stream);
+epl_status epl_debug_f32_to_bf16(const float *in, uint16_t *out, int64_t n, void *stream);
+
+/* Static strings; never NULL. */
+const char *epl_status_str(epl_status status);
+const char *epl_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EPL_H */

@@ -1,0 +1,144 @@
+// C ABI of libepl: host-side argument checks, layout geometry, workspace sizing and kernel
+// launches on the caller's stream. Stateless and reentrant; allocates nothing.
+#include <limits.h>
+
+#include "epl_internal.h"
+
+#define EPL_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+int bits_for(int n) {  // bits needed to represent values 0..n-1
+  int b = 0;
+  while ((1 << b) < n) ++b;
+  return b;
+}
+
+// Common config checks; EPL_OK if the shape is one the library handles.
+epl_status check_config(const epl_config* cfg) {
+  if (!cfg) return EPL_ERR_INVALID_ARG;
+  const int R = cfg->num_ranks, E = cfg->num_experts, k = cfg->topk, H = cfg->hidden, Tr = cfg->tokens_per_rank;
+  if (R < 1 || E < R || E > EPL_MAX_EXPERTS || E % R != 0) return EPL_ERR_INVALID_ARG;
+  if (k < 1 || k > EPL_MAX_TOPK || Tr < 0 || H < 8 || H % 8 != 0) return EPL_ERR_INVALID_ARG;
+  if ((int64_t)R * Tr * k >= (int64_t)INT_MAX) return EPL_ERR_INVALID_ARG;
+  if (cfg->payload != EPL_PAYLOAD_BF16 && cfg->payload != EPL_PAYLOAD_FP8_E4M3) return EPL_ERR_UNSUPPORTED;
+  return EPL_OK;
+}
+
+// Chunking of each source rank's tokens for the layout kernels: whole tokens, at most
+// kMaxChunkPairs pairs per workgroup.
+epl::Geom make_geom(const epl_config* cfg) {
+  epl::Geom g;
+  g.R = cfg->num_ranks;
+  g.E = cfg->num_experts;
+  g.El = g.E / g.R;
+  g.k = cfg->topk;
+  g.Tr = cfg->tokens_per_rank;
+  g.T = (int64_t)g.R * g.Tr;
+  const int cap = epl::kMaxChunkPairs / g.k;  // k <= 32 so cap >= 32
+  g.CT = g.Tr < 1 ? 1 : (g.Tr < cap ? g.Tr : cap);
+  g.NC = g.Tr < 1 ? 1 : (g.Tr + g.CT - 1) / g.CT;
+  g.nblk = g.R * g.NC;
+  g.ebits = bits_for(g.E);
+  g.rbits = bits_for(g.R);
+  return g;
+}
+
+size_t workspace_bytes(const epl::Geom& g) { return epl::ws_layout(g).total * sizeof(int32_t); }
+
+epl_status check_layout_buffers(const epl_layout_buffers* L) {
+  if (!L) return EPL_ERR_INVALID_ARG;
+  int32_t* const ptrs[] = {L->send_cnt, L->rank_cnt, L->expert_off, L->rank_off, L->seg_off, L->tok_nranks,
+                           L->pair_row, L->pair_rslot, L->recv_src,  L->recv_j,   L->num_invalid};
+  for (int32_t* p : ptrs) {
+    if (!p) return EPL_ERR_INVALID_ARG;
+    if (!aligned(p, 4)) return EPL_ERR_ALIGN;
+  }
+  return EPL_OK;
+}
+
+epl_status from_hip(hipError_t e) { return e == hipSuccess ? EPL_OK : EPL_ERR_DEVICE; }
+
+}  // namespace
+
+EPL_EXPORT size_t epl_workspace_bytes(const epl_config* cfg) {
+  if (check_config(cfg) != EPL_OK) return 0;
+  return workspace_bytes(make_geom(cfg));
+}
+
+EPL_EXPORT epl_status epl_layout(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                 void* workspace, size_t ws_bytes, void* stream) {
+  epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  if ((st = check_layout_buffers(L)) != EPL_OK) return st;
+  const epl::Geom g = make_geom(cfg);
+  if (g.T > 0 && !topk_idx) return EPL_ERR_INVALID_ARG;
+  if (!aligned(topk_idx, 4)) return EPL_ERR_ALIGN;
+  if (!workspace) return EPL_ERR_WORKSPACE;
+  if (!aligned(workspace, 4)) return EPL_ERR_ALIGN;
+  if (ws_bytes < workspace_bytes(g)) return EPL_ERR_WORKSPACE;
+  return from_hip(epl::launch_layout(g, topk_idx, static_cast<int32_t*>(workspace), L->send_cnt, L->rank_cnt,
+                                     L->expert_off, L->rank_off, L->seg_off, L->tok_nranks, L->pair_row,
+                                     L->pair_rslot, L->recv_src, L->recv_j, L->num_invalid,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT epl_status epl_dispatch(const epl_config* cfg, const void* x, const epl_layout_buffers* L, void* recv,
+                                   float* recv_scale, int64_t recv_rows_cap, void* stream) {
+  epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  const bool fp8 = cfg->payload == EPL_PAYLOAD_FP8_E4M3;
+  if (fp8 && cfg->hidden % 128 != 0) return EPL_ERR_UNSUPPORTED;
+  if (!L || !L->pair_row) return EPL_ERR_INVALID_ARG;
+  if (!aligned(L->pair_row, 4)) return EPL_ERR_ALIGN;
+  const int64_t T = (int64_t)cfg->num_ranks * cfg->tokens_per_rank;
+  if (T > 0 && (!x || !recv || (fp8 && !recv_scale))) return EPL_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(recv, 16) || (fp8 && !aligned(recv_scale, 4))) return EPL_ERR_ALIGN;
+  if (recv_rows_cap < T * cfg->topk) return EPL_ERR_CAPACITY;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (fp8) return from_hip(epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, T, cfg->topk, cfg->hidden,
+                                                   recv_rows_cap, s));
+  return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, T, cfg->topk, cfg->hidden, recv_rows_cap, s));
+}
+
+EPL_EXPORT epl_status epl_combine(const epl_config* cfg, const void* y, const float* topk_w,
+                                  const epl_layout_buffers* L, void* out, void* stream) {
+  epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  if (!L || !L->pair_row) return EPL_ERR_INVALID_ARG;
+  if (!aligned(L->pair_row, 4)) return EPL_ERR_ALIGN;
+  const int64_t T = (int64_t)cfg->num_ranks * cfg->tokens_per_rank;
+  if (T > 0 && (!y || !topk_w || !out)) return EPL_ERR_INVALID_ARG;
+  if (!aligned(y, 16) || !aligned(out, 16) || !aligned(topk_w, 4)) return EPL_ERR_ALIGN;
+  return from_hip(epl::launch_combine(y, topk_w, L->pair_row, out, T, cfg->topk, cfg->hidden,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT epl_status epl_debug_f32_to_e4m3(const float* in, uint8_t* out, int64_t n, void* stream) {
+  if (n < 0 || (n > 0 && (!in || !out))) return EPL_ERR_INVALID_ARG;
+  if (!aligned(in, 4) || !aligned(out, 4)) return EPL_ERR_ALIGN;
+  return from_hip(epl::launch_debug_e4m3(in, out, n, static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT epl_status epl_debug_f32_to_bf16(const float* in, uint16_t* out, int64_t n, void* stream) {
+  if (n < 0 || (n > 0 && (!in || !out))) return EPL_ERR_INVALID_ARG;
+  if (!aligned(in, 4) || !aligned(out, 4)) return EPL_ERR_ALIGN;
+  return from_hip(epl::launch_debug_bf16(in, out, n, static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT const char* epl_status_str(epl_status s) {
+  switch (s) {
+    case EPL_OK: return "EPL_OK";
+    case EPL_ERR_INVALID_ARG: return "EPL_ERR_INVALID_ARG: invalid argument";
+    case EPL_ERR_ALIGN: return "EPL_ERR_ALIGN: misaligned pointer";
+    case EPL_ERR_CAPACITY: return "EPL_ERR_CAPACITY: recv_rows_cap < T*k";
+    case EPL_ERR_WORKSPACE: return "EPL_ERR_WORKSPACE: workspace too small";
+    case EPL_ERR_UNSUPPORTED: return "EPL_ERR_UNSUPPORTED: unsupported payload or hidden size";
+    case EPL_ERR_DEVICE: return "EPL_ERR_DEVICE: HIP runtime error";
+  }
+  return "EPL: unknown status";
+}
+
+EPL_EXPORT const char* epl_version(void) { return "epl 0.1.0 (gfx950)"; }

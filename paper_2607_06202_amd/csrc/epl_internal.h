@@ -1,0 +1,154 @@
+// Internal declarations shared by the epl HIP sources (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "epl.h"
+
+namespace epl {
+
+constexpr int kWave = 64;
+constexpr int kLayoutThreads = 256;
+constexpr int kLayoutWaves = kLayoutThreads / kWave;
+// Pairs handled by one layout workgroup ("chunk"); a chunk never spans two source ranks and
+// always holds whole tokens.
+constexpr int kMaxChunkPairs = 1024;
+constexpr int kChunkSlots = kMaxChunkPairs / kLayoutThreads;  // register slots per lane
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Shape of one layout problem, derived on the host from epl_config.
+struct Geom {
+  int R, E, El, k, Tr;
+  int CT;     // tokens per chunk
+  int NC;     // chunks per source rank (>= 1)
+  int nblk;   // R * NC layout workgroups
+  int ebits;  // bits needed for an expert id (ballot-match key width)
+  int rbits;  // bits needed for a rank id
+  int64_t T;
+};
+
+// Workspace carve-up, in int32 elements.
+struct WsLayout {
+  size_t chunk_e;   // [E][nblk]  per-chunk expert counts, then chunk base rows within the expert
+  size_t chunk_r;   // [nblk][R]  per-chunk first-pair counts per destination rank, then slot bases
+  size_t recv_cnt;  // [E]
+  size_t inval;     // [nblk]
+  size_t total;
+};
+
+inline WsLayout ws_layout(const Geom& g) {
+  WsLayout w;
+  size_t o = 0;
+  w.chunk_e = o;
+  o += (size_t)g.E * g.nblk;
+  w.chunk_r = o;
+  o += (size_t)g.nblk * g.R;
+  w.recv_cnt = o;
+  o += (size_t)g.E;
+  w.inval = o;
+  o += (size_t)g.nblk;
+  w.total = o;
+  return w;
+}
+
+// ---------------------------------------------------------------- wave64 primitives
+__device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0)); }
+
+// popcount(mask & lanes-below-me): a lane's rank among the lanes of `mask`.
+__device__ __forceinline__ int rank_in_mask(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
+
+// Lanes of the wave that are active and hold the same `key` as this lane (match-any built
+// from one ballot per key bit). `nbits` must be wave-uniform. Result is meaningless for an
+// inactive lane.
+__device__ __forceinline__ uint64_t match_key(bool active, int key, int nbits) {
+  uint64_t m = __ballot(active);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = (key >> b) & 1;
+    const uint64_t bb = __ballot(active && bit);
+    m &= bit ? bb : ~bb;
+  }
+  return m;
+}
+
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int t = __shfl_up(v, off, kWave);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Exclusive prefix sum across a 256-thread block; `total` receives the block sum. Every
+// thread of the block must call it (it synchronises).
+__device__ __forceinline__ int block_exclusive_sum(int v, int& total, int* scratch /* [kLayoutWaves] */) {
+  const int inc = wave_inclusive_sum(v);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == kWave - 1) scratch[w] = inc;
+  __syncthreads();
+  int pre = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kLayoutWaves; ++i) {
+    const int s = scratch[i];
+    pre += (i < w) ? s : 0;
+    tot += s;
+  }
+  __syncthreads();
+  total = tot;
+  return pre + inc - v;
+}
+
+// ---------------------------------------------------------------- number conversions
+// Four fp32 values -> four OCP E4M3 bytes (byte i from argument i), round to nearest even,
+// magnitudes above 448 saturated to 448 (the clamp is exact and RNE never rounds a value
+// below 464 past 448), sign kept on zero.
+__device__ __forceinline__ uint32_t f32x4_to_e4m3x4(float a, float b, float c, float d) {
+  a = __builtin_amdgcn_fmed3f(a, 448.0f, -448.0f);
+  b = __builtin_amdgcn_fmed3f(b, 448.0f, -448.0f);
+  c = __builtin_amdgcn_fmed3f(c, 448.0f, -448.0f);
+  d = __builtin_amdgcn_fmed3f(d, 448.0f, -448.0f);
+  const uint32_t lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0u, false);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
+}
+
+// Two fp32 -> packed bf16x2 (low half from `lo`), round to nearest even.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float lo, float hi) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const f32x2 f = {lo, hi};
+  const bf16x2 b = __builtin_convertvector(f, bf16x2);
+  return __builtin_bit_cast(uint32_t, b);
+}
+
+__device__ __forceinline__ float bf16lo_to_f32(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// ---------------------------------------------------------------- launchers (host side)
+hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
+                         int32_t* expert_off, int32_t* rank_off, int32_t* seg_off, int32_t* tok_nranks,
+                         int32_t* pair_row, int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j,
+                         int32_t* num_invalid, hipStream_t stream);
+
+hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* recv, int64_t T, int k, int H,
+                                int64_t cap, hipStream_t stream);
+hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* recv, float* recv_scale, int64_t T,
+                               int k, int H, int64_t cap, hipStream_t stream);
+hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
+                          int H, hipStream_t stream);
+
+hipError_t launch_debug_e4m3(const float* in, uint8_t* out, int64_t n, hipStream_t stream);
+hipError_t launch_debug_bf16(const float* in, uint16_t* out, int64_t n, hipStream_t stream);
+
+}  // namespace epl

@@ -1,0 +1,357 @@
+// Routing layout for MoE dispatch on one GPU: per-(source rank, expert) histograms, CalCumSum
+// prefix scans, stable packed-row assignment and per-token destination-rank dedup.
+//
+// The paper's dispatch reports per-expert token counts from every source. Prefix sums of those
+// counts give each expert's HBM offsets, and tokens are then laid out contiguously per expert
+// (Background phases 3 and 5; Kernel Decomposition: TokenCnt-Sending, CalCumSum,
+// Token-Reordering). All ranks are virtual here, so the count "exchange" is just reading the
+// [rank][expert] matrix by column.
+//
+// Three launches, no atomics that decide an order, bit-identical on every run:
+//   K1 route_hist      one workgroup per chunk (CT whole tokens of one source rank): LDS
+//                      histograms of expert ids and of first-per-token destination ranks,
+//                      tok_nranks, invalid count.
+//   K2 route_scan      one workgroup per expert column: scan over (source rank, chunk) giving
+//                      seg_off (relative to the expert start), send_cnt, recv_cnt and per-chunk
+//                      base rows. One workgroup per source rank: scan of rank slots over chunks.
+//                      One workgroup: num_invalid.
+//   K3 route_finalize  one workgroup per chunk: expert_off via an LDS scan of recv_cnt. Each
+//                      wave takes a contiguous quarter of the chunk's pairs and gives every pair
+//                      its stable rank among equal keys: ballot match over the key bits,
+//                      popcount of the lanes below, per-wave LDS running counts. A cross-wave
+//                      prefix then yields pair_row, recv_src, recv_j and pair_rslot.
+#include "epl_internal.h"
+
+namespace epl {
+
+// ------------------------------------------------------------------------------------ K1
+__global__ void __launch_bounds__(kLayoutThreads)
+    route_hist_kernel(Geom G, const int32_t* __restrict__ idx, int32_t* __restrict__ tok_nranks,
+                      int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r, int32_t* __restrict__ inval) {
+  extern __shared__ int32_t lds[];
+  int32_t* hist_e = lds;          // [E]
+  int32_t* hist_r = hist_e + G.E;  // [R]
+  int32_t* dst = hist_r + G.R;     // [kMaxChunkPairs] destination rank of each pair, -1 if invalid
+  __shared__ int32_t red[kLayoutWaves];
+
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const int s = b / G.NC;
+  const int c = b - s * G.NC;
+  const int t0 = c * G.CT;
+  const int nt = max(0, min(G.CT, G.Tr - t0));
+  const int np = nt * G.k;
+  const int64_t g0 = (int64_t)s * G.Tr + t0;
+
+  for (int i = tid; i < G.E + G.R; i += kLayoutThreads) lds[i] = 0;
+  __syncthreads();
+
+  const int32_t* src = idx + g0 * G.k;
+  int my_inval = 0;
+  for (int i = tid; i < np; i += kLayoutThreads) {
+    const int e = src[i];
+    const bool ok = (unsigned)e < (unsigned)G.E;
+    dst[i] = ok ? e / G.El : -1;
+    if (ok)
+      atomicAdd(&hist_e[e], 1);
+    else
+      ++my_inval;
+  }
+  __syncthreads();
+
+  // Dedup: a pair is the first of its token for its destination rank if no earlier valid pair
+  // of the token targets the same rank. One thread per token.
+  for (int t = tid; t < nt; t += kLayoutThreads) {
+    const int32_t* dt = dst + t * G.k;
+    int nr = 0;
+    for (int j = 0; j < G.k; ++j) {
+      const int d = dt[j];
+      if (d < 0) continue;
+      bool first = true;
+      for (int jj = 0; jj < j; ++jj) first &= (dt[jj] != d);
+      if (first) {
+        atomicAdd(&hist_r[d], 1);
+        ++nr;
+      }
+    }
+    tok_nranks[g0 + t] = nr;
+  }
+
+  const int wsum = wave_sum(my_inval);
+  if (lane_id() == 0) red[tid / kWave] = wsum;
+  __syncthreads();
+
+  for (int e = tid; e < G.E; e += kLayoutThreads) chunk_e[(int64_t)e * G.nblk + b] = hist_e[e];
+  for (int r = tid; r < G.R; r += kLayoutThreads) chunk_r[(int64_t)b * G.R + r] = hist_r[r];
+  if (tid == 0) {
+    int n = 0;
+    for (int w = 0; w < kLayoutWaves; ++w) n += red[w];
+    inval[b] = n;
+  }
+}
+
+// ------------------------------------------------------------------------------------ K2
+__global__ void __launch_bounds__(kLayoutThreads)
+    route_scan_kernel(Geom G, int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r,
+                      const int32_t* __restrict__ inval, int32_t* __restrict__ recv_cnt, int32_t* __restrict__ send_cnt,
+                      int32_t* __restrict__ rank_cnt, int32_t* __restrict__ seg_off, int32_t* __restrict__ num_invalid) {
+  __shared__ int32_t scratch[kLayoutWaves];
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  if (b < G.E) {
+    // Expert column e, laid out [source rank][chunk]: counts -> rows relative to the expert start.
+    const int e = b;
+    int32_t* col = chunk_e + (int64_t)e * G.nblk;
+    int carry = 0;
+    for (int s0 = 0; s0 < G.R; s0 += kLayoutThreads) {
+      const int s = s0 + tid;
+      int sum = 0;
+      if (s < G.R)
+        for (int c = 0; c < G.NC; ++c) sum += col[s * G.NC + c];
+      int total;
+      const int excl = block_exclusive_sum(sum, total, scratch);
+      if (s < G.R) {
+        const int base = carry + excl;
+        seg_off[(int64_t)e * G.R + s] = base;  // K3 adds expert_off[e]
+        send_cnt[(int64_t)s * G.E + e] = sum;
+        int run = base;
+        for (int c = 0; c < G.NC; ++c) {
+          const int h = col[s * G.NC + c];
+          col[s * G.NC + c] = run;
+          run += h;
+        }
+      }
+      carry += total;
+    }
+    if (tid == 0) recv_cnt[e] = carry;
+  } else if (b < G.E + G.R) {
+    // Source rank s: per destination rank r, slots of earlier chunks come first.
+    const int s = b - G.E;
+    for (int r = tid; r < G.R; r += kLayoutThreads) {
+      int run = 0;
+      for (int c = 0; c < G.NC; ++c) {
+        int32_t* p = chunk_r + (int64_t)(s * G.NC + c) * G.R + r;
+        const int h = *p;
+        *p = run;
+        run += h;
+      }
+      rank_cnt[(int64_t)s * G.R + r] = run;
+    }
+  } else {
+    int n = 0;
+    for (int i = tid; i < G.nblk; i += kLayoutThreads) n += inval[i];
+    const int w = wave_sum(n);
+    if (lane_id() == 0) scratch[tid / kWave] = w;
+    __syncthreads();
+    if (tid == 0) {
+      int t = 0;
+      for (int i = 0; i < kLayoutWaves; ++i) t += scratch[i];
+      num_invalid[0] = t;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------ K3
+__global__ void __launch_bounds__(kLayoutThreads)
+    route_finalize_kernel(Geom G, const int32_t* __restrict__ idx, const int32_t* __restrict__ chunk_e,
+                          const int32_t* __restrict__ chunk_r, const int32_t* __restrict__ recv_cnt,
+                          int32_t* __restrict__ expert_off, int32_t* __restrict__ rank_off, int32_t* __restrict__ seg_off,
+                          int32_t* __restrict__ pair_row, int32_t* __restrict__ pair_rslot, int32_t* __restrict__ recv_src,
+                          int32_t* __restrict__ recv_j) {
+  extern __shared__ int32_t lds[];
+  int32_t* eoff = lds;                               // [E+1]
+  int32_t* base_e = eoff + G.E + 1;                  // [E]   first packed row of this chunk's pairs of expert e
+  int32_t* base_r = base_e + G.E;                    // [R]   first slot of this chunk's tokens bound for rank r
+  int32_t* whe = base_r + G.R;                       // [W][E] per-wave counts, then per-wave bases
+  int32_t* whr = whe + kLayoutWaves * G.E;           // [W][R]
+  int32_t* ekey = whr + kLayoutWaves * G.R;          // [kMaxChunkPairs] expert id, -1 invalid
+  int32_t* dkey = ekey + kMaxChunkPairs;             // [kMaxChunkPairs] destination rank, -1 invalid
+  int32_t* rs = dkey + kMaxChunkPairs;               // [kMaxChunkPairs] slot of first pairs
+  __shared__ int32_t scratch[kLayoutWaves];
+
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const int s = b / G.NC;
+  const int c = b - s * G.NC;
+  const int t0 = c * G.CT;
+  const int nt = max(0, min(G.CT, G.Tr - t0));
+  const int np = nt * G.k;
+  const int64_t g0 = (int64_t)s * G.Tr + t0;
+
+  const int32_t* src = idx + g0 * G.k;
+  for (int i = tid; i < np; i += kLayoutThreads) {
+    const int e = src[i];
+    const bool ok = (unsigned)e < (unsigned)G.E;
+    ekey[i] = ok ? e : -1;
+    dkey[i] = ok ? e / G.El : -1;
+  }
+  for (int i = tid; i < kLayoutWaves * (G.E + G.R); i += kLayoutThreads) whe[i] = 0;
+
+  // expert_off = exclusive scan of recv_cnt; each thread owns a contiguous run of experts.
+  {
+    const int per = (G.E + kLayoutThreads - 1) / kLayoutThreads;
+    const int e0 = min(G.E, tid * per), e1 = min(G.E, e0 + per);
+    int sum = 0;
+    for (int e = e0; e < e1; ++e) sum += recv_cnt[e];
+    int total;
+    int run = block_exclusive_sum(sum, total, scratch);
+    for (int e = e0; e < e1; ++e) {
+      eoff[e] = run;
+      run += recv_cnt[e];
+    }
+    if (tid == 0) eoff[G.E] = total;
+  }
+  __syncthreads();
+
+  for (int e = tid; e < G.E; e += kLayoutThreads) base_e[e] = eoff[e] + chunk_e[(int64_t)e * G.nblk + b];
+  for (int r = tid; r < G.R; r += kLayoutThreads) base_r[r] = chunk_r[(int64_t)b * G.R + r];
+  if (b == 0) {
+    for (int e = tid; e <= G.E; e += kLayoutThreads) expert_off[e] = eoff[e];
+    for (int d = tid; d <= G.R; d += kLayoutThreads) rank_off[d] = eoff[d * G.El];
+  }
+  {
+    // seg_off holds offsets relative to the expert start; each workgroup rebases one slice.
+    const int64_t n = (int64_t)G.E * G.R;
+    const int64_t per = (n + G.nblk - 1) / G.nblk;
+    const int64_t i0 = (int64_t)b * per, i1 = min(n, i0 + per);
+    for (int64_t i = i0 + tid; i < i1; i += kLayoutThreads) seg_off[i] += eoff[i / G.R];
+  }
+  __syncthreads();
+
+  // Stable ranks. Wave w owns pairs [w*Q, w*Q + Q) of the chunk, walked 64 at a time in pair
+  // order; whe/whr[w][key] count the keys this wave has already seen.
+  const int w = tid / kWave;
+  const int lane = tid - w * kWave;
+  const int Q = ((np + kLayoutThreads - 1) / kLayoutThreads) * kWave;
+  const int p_beg = w * Q;
+  const int p_end = min(np, p_beg + Q);
+  int rank_e[kChunkSlots], rank_r[kChunkSlots];
+  uint32_t first_bits = 0;
+#pragma unroll
+  for (int it = 0; it < kChunkSlots; ++it) {
+    rank_e[it] = 0;
+    rank_r[it] = 0;
+    if (p_beg + it * kWave >= p_end) continue;  // wave-uniform
+    const int p = p_beg + it * kWave + lane;
+    const bool active = p < p_end;
+    const int e = active ? ekey[p] : -1;
+    const int d = active ? dkey[p] : -1;
+    const bool valid = e >= 0;
+    bool first = valid;
+    if (valid) {
+      const int t = p / G.k;
+      const int j = p - t * G.k;
+      for (int jj = 0; jj < j; ++jj) first &= (dkey[t * G.k + jj] != d);
+    }
+    first_bits |= first ? (1u << it) : 0u;
+
+    const uint64_t me = match_key(valid, e, G.ebits);
+    const int lo_e = rank_in_mask(me);
+    const int cnt_e = __popcll(me);
+    const int seen_e = valid ? whe[w * G.E + e] : 0;
+    if (valid && lo_e == 0) whe[w * G.E + e] = seen_e + cnt_e;  // one lane per key
+    rank_e[it] = seen_e + lo_e;
+
+    const uint64_t mr = match_key(first, d, G.rbits);
+    const int lo_r = rank_in_mask(mr);
+    const int cnt_r = __popcll(mr);
+    const int seen_r = first ? whr[w * G.R + d] : 0;
+    if (first && lo_r == 0) whr[w * G.R + d] = seen_r + cnt_r;
+    rank_r[it] = seen_r + lo_r;
+  }
+  __syncthreads();
+
+  // Per-wave counts -> per-wave bases (exclusive prefix over waves, in wave order).
+  for (int e = tid; e < G.E; e += kLayoutThreads) {
+    int run = 0;
+#pragma unroll
+    for (int v = 0; v < kLayoutWaves; ++v) {
+      const int h = whe[v * G.E + e];
+      whe[v * G.E + e] = run;
+      run += h;
+    }
+  }
+  for (int r = tid; r < G.R; r += kLayoutThreads) {
+    int run = 0;
+#pragma unroll
+    for (int v = 0; v < kLayoutWaves; ++v) {
+      const int h = whr[v * G.R + r];
+      whr[v * G.R + r] = run;
+      run += h;
+    }
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int it = 0; it < kChunkSlots; ++it) {
+    if (p_beg + it * kWave >= p_end) continue;
+    const int p = p_beg + it * kWave + lane;
+    if (p >= p_end) continue;
+    const int e = ekey[p];
+    const int t = p / G.k;
+    const int j = p - t * G.k;
+    const int64_t g = g0 + t;
+    if (e >= 0) {
+      const int row = base_e[e] + whe[w * G.E + e] + rank_e[it];
+      pair_row[g * G.k + j] = row;
+      if (row < eoff[G.E]) {  // always true for a consistent layout; keeps stores in bounds
+        recv_src[row] = (int32_t)g;
+        recv_j[row] = j;
+      }
+    } else {
+      pair_row[g * G.k + j] = -1;
+    }
+    if (first_bits & (1u << it)) {
+      const int d = dkey[p];
+      rs[p] = base_r[d] + whr[w * G.R + d] + rank_r[it];
+    }
+  }
+  __syncthreads();
+
+  // Every valid pair reports the slot of its token's first pair on the same rank.
+  for (int p = tid; p < np; p += kLayoutThreads) {
+    const int d = dkey[p];
+    const int t = p / G.k;
+    int slot = -1;
+    if (d >= 0) {
+      int jf = t * G.k;
+      while (dkey[jf] != d) ++jf;
+      slot = rs[jf];
+    }
+    pair_rslot[(g0 + t) * G.k + (p - t * G.k)] = slot;
+  }
+}
+
+// ------------------------------------------------------------------------------------ host
+static size_t finalize_lds_bytes(const Geom& g) {
+  return sizeof(int32_t) * ((size_t)(g.E + 1) + g.E + g.R + (size_t)kLayoutWaves * (g.E + g.R) + 3 * kMaxChunkPairs);
+}
+
+hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
+                         int32_t* expert_off, int32_t* rank_off, int32_t* seg_off, int32_t* tok_nranks,
+                         int32_t* pair_row, int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j,
+                         int32_t* num_invalid, hipStream_t stream) {
+  const WsLayout wl = ws_layout(g);
+  int32_t* chunk_e = ws + wl.chunk_e;
+  int32_t* chunk_r = ws + wl.chunk_r;
+  int32_t* recv_cnt = ws + wl.recv_cnt;
+  int32_t* inval = ws + wl.inval;
+
+  const size_t lds1 = sizeof(int32_t) * ((size_t)g.E + g.R + kMaxChunkPairs);
+  hipLaunchKernelGGL(route_hist_kernel, dim3(g.nblk), dim3(kLayoutThreads), lds1, stream, g, idx, tok_nranks,
+                     chunk_e, chunk_r, inval);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+
+  hipLaunchKernelGGL(route_scan_kernel, dim3(g.E + g.R + 1), dim3(kLayoutThreads), 0, stream, g, chunk_e, chunk_r,
+                     inval, recv_cnt, send_cnt, rank_cnt, seg_off, num_invalid);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+
+  hipLaunchKernelGGL(route_finalize_kernel, dim3(g.nblk), dim3(kLayoutThreads), finalize_lds_bytes(g), stream, g,
+                     idx, chunk_e, chunk_r, recv_cnt, expert_off, rank_off, seg_off, pair_row, pair_rslot, recv_src,
+                     recv_j);
+  return hipGetLastError();
+}
+
+}  // namespace epl

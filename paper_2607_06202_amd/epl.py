@@ -1,0 +1,220 @@
+"""Python binding of libepl (MoE dispatch / combine on one MI355X): argument marshalling only.
+
+Every step runs in the HIP kernels behind the C ABI declared in ``include/epl.h``. This module
+allocates output tensors with torch on the tensors' device, passes raw device pointers and the
+current HIP stream, and turns status codes into exceptions. There is no fallback: if
+``libepl.so`` is missing, or a tensor is not on the GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libepl.so")
+
+PAYLOAD_BF16 = 0
+PAYLOAD_FP8_E4M3 = 1
+MAX_EXPERTS = 1024
+MAX_TOPK = 32
+
+STATUS = {0: "EPL_OK", 1: "EPL_ERR_INVALID_ARG", 2: "EPL_ERR_ALIGN", 3: "EPL_ERR_CAPACITY",
+          4: "EPL_ERR_WORKSPACE", 5: "EPL_ERR_UNSUPPORTED", 6: "EPL_ERR_DEVICE"}
+
+
+class EplError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s" % (what, STATUS.get(status, status)))
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("num_ranks", ctypes.c_int32), ("num_experts", ctypes.c_int32), ("topk", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("tokens_per_rank", ctypes.c_int32), ("payload", ctypes.c_int32)]
+
+    @property
+    def T(self) -> int:
+        return self.num_ranks * self.tokens_per_rank
+
+    def __repr__(self) -> str:
+        return "Config(R=%d, E=%d, k=%d, H=%d, Tr=%d, payload=%d)" % (
+            self.num_ranks, self.num_experts, self.topk, self.hidden, self.tokens_per_rank, self.payload)
+
+
+def config(R: int, E: int, k: int, H: int, Tr: int, payload: str | int = "bf16") -> Config:
+    if isinstance(payload, str):
+        payload = {"bf16": PAYLOAD_BF16, "fp8": PAYLOAD_FP8_E4M3}[payload]
+    return Config(R, E, k, H, Tr, payload)
+
+
+class LayoutBuffers(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("send_cnt", "rank_cnt", "expert_off", "rank_off", "seg_off",
+                                               "tok_nranks", "pair_row", "pair_rslot", "recv_src", "recv_j",
+                                               "num_invalid")]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libepl.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libepl.so is not built (run __graft_entry__.build()): %s" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, I64, S = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+        CP, LP = ctypes.POINTER(Config), ctypes.POINTER(LayoutBuffers)
+        L.epl_workspace_bytes.restype = S
+        L.epl_workspace_bytes.argtypes = [CP]
+        L.epl_layout.restype = ctypes.c_int
+        L.epl_layout.argtypes = [CP, P, LP, P, S, P]
+        L.epl_dispatch.restype = ctypes.c_int
+        L.epl_dispatch.argtypes = [CP, P, LP, P, P, I64, P]
+        L.epl_combine.restype = ctypes.c_int
+        L.epl_combine.argtypes = [CP, P, P, LP, P, P]
+        L.epl_debug_f32_to_e4m3.restype = ctypes.c_int
+        L.epl_debug_f32_to_e4m3.argtypes = [P, P, I64, P]
+        L.epl_debug_f32_to_bf16.restype = ctypes.c_int
+        L.epl_debug_f32_to_bf16.argtypes = [P, P, I64, P]
+        L.epl_status_str.restype = ctypes.c_char_p
+        L.epl_status_str.argtypes = [ctypes.c_int]
+        L.epl_version.restype = ctypes.c_char_p
+        L.epl_version.argtypes = []
+        _lib = L
+    return _lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != 0:
+        raise EplError(status, what)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None) -> int:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    return t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def workspace_bytes(cfg: Config) -> int:
+    return int(lib().epl_workspace_bytes(ctypes.byref(cfg)))
+
+
+@dataclass
+class Layout:
+    """Device outputs of epl_layout (int32 tensors)."""
+    cfg: Config
+    send_cnt: torch.Tensor    # [R, E]
+    rank_cnt: torch.Tensor    # [R, R]
+    expert_off: torch.Tensor  # [E+1]
+    rank_off: torch.Tensor    # [R+1]
+    seg_off: torch.Tensor     # [E, R]
+    tok_nranks: torch.Tensor  # [T]
+    pair_row: torch.Tensor    # [T, k]
+    pair_rslot: torch.Tensor  # [T, k]
+    recv_src: torch.Tensor    # [T*k] (first P valid)
+    recv_j: torch.Tensor      # [T*k] (first P valid)
+    num_invalid: torch.Tensor  # [1]
+    workspace: torch.Tensor   # uint8 scratch
+
+    def buffers(self) -> LayoutBuffers:
+        return LayoutBuffers(*[getattr(self, n).data_ptr() for n, _ in LayoutBuffers._fields_])
+
+
+def alloc_layout(cfg: Config, device) -> Layout:
+    R, E, k, T = cfg.num_ranks, cfg.num_experts, cfg.topk, cfg.T
+    i32 = dict(dtype=torch.int32, device=device)
+    ws = workspace_bytes(cfg)
+    if ws == 0:
+        raise EplError(1, "epl_workspace_bytes(%r)" % (cfg,))
+    return Layout(cfg, torch.empty(R, E, **i32), torch.empty(R, R, **i32), torch.empty(E + 1, **i32),
+                  torch.empty(R + 1, **i32), torch.empty(E, R, **i32), torch.empty(max(T, 1), **i32),
+                  torch.empty(max(T, 1), k, **i32), torch.empty(max(T, 1), k, **i32), torch.empty(max(T * k, 1), **i32),
+                  torch.empty(max(T * k, 1), **i32), torch.empty(1, **i32),
+                  torch.empty(ws, dtype=torch.uint8, device=device))
+
+
+def layout(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> Layout:
+    """epl_layout: topk_idx [T, k] int32 on the GPU -> Layout."""
+    dev = topk_idx.device
+    _dev(topk_idx, "topk_idx", torch.int32)
+    if topk_idx.numel() != cfg.T * cfg.topk:
+        raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
+    L = out if out is not None else alloc_layout(cfg, dev)
+    bufs = L.buffers()
+    _check(lib().epl_layout(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs), L.workspace.data_ptr(),
+                            L.workspace.numel(), _stream(dev)), "epl_layout")
+    return L
+
+
+def recv_rows_cap(cfg: Config) -> int:
+    return cfg.T * cfg.topk
+
+
+def alloc_recv(cfg: Config, device, rows: int | None = None):
+    rows = recv_rows_cap(cfg) if rows is None else rows
+    if cfg.payload == PAYLOAD_FP8_E4M3:
+        return (torch.empty(max(rows, 1), cfg.hidden, dtype=torch.uint8, device=device),
+                torch.empty(max(rows, 1), cfg.hidden // 128, dtype=torch.float32, device=device))
+    return torch.empty(max(rows, 1), cfg.hidden, dtype=torch.bfloat16, device=device), None
+
+
+def dispatch(cfg: Config, x: torch.Tensor, L: Layout, recv: torch.Tensor | None = None,
+             recv_scale: torch.Tensor | None = None):
+    """epl_dispatch: x [T, H] bf16 -> (recv [cap, H] bf16 | uint8, recv_scale [cap, H/128] fp32 | None)."""
+    dev = x.device
+    _dev(x, "x", torch.bfloat16)
+    if recv is None:
+        recv, recv_scale = alloc_recv(cfg, dev)
+    fp8 = cfg.payload == PAYLOAD_FP8_E4M3
+    _dev(recv, "recv", torch.uint8 if fp8 else torch.bfloat16)
+    sp = _dev(recv_scale, "recv_scale", torch.float32) if fp8 else None
+    bufs = L.buffers()
+    _check(lib().epl_dispatch(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(), sp,
+                              recv.shape[0] if recv.numel() else 0, _stream(dev)), "epl_dispatch")
+    return recv, recv_scale
+
+
+def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):
+    """epl_combine: y [>=P, H] bf16, topk_w [T, k] fp32 -> out [T, H] bf16."""
+    dev = y.device
+    _dev(y, "y", torch.bfloat16)
+    _dev(topk_w, "topk_w", torch.float32)
+    if out is None:
+        out = torch.empty(max(cfg.T, 1), cfg.hidden, dtype=torch.bfloat16, device=dev)
+    _dev(out, "out", torch.bfloat16)
+    bufs = L.buffers()
+    _check(lib().epl_combine(ctypes.byref(cfg), y.data_ptr(), topk_w.data_ptr(), ctypes.byref(bufs), out.data_ptr(),
+                             _stream(dev)), "epl_combine")
+    return out
+
+
+def debug_f32_to_e4m3(v: torch.Tensor) -> torch.Tensor:
+    _dev(v, "v", torch.float32)
+    out = torch.empty(v.numel(), dtype=torch.uint8, device=v.device)
+    _check(lib().epl_debug_f32_to_e4m3(v.data_ptr(), out.data_ptr(), v.numel(), _stream(v.device)),
+           "epl_debug_f32_to_e4m3")
+    return out
+
+
+def debug_f32_to_bf16(v: torch.Tensor) -> torch.Tensor:
+    _dev(v, "v", torch.float32)
+    out = torch.empty(v.numel(), dtype=torch.int16, device=v.device)
+    _check(lib().epl_debug_f32_to_bf16(v.data_ptr(), out.data_ptr(), v.numel(), _stream(v.device)),
+           "epl_debug_f32_to_bf16")
+    return out
+
+
+def version() -> str:
+    return lib().epl_version().decode()

@@ -1,0 +1,152 @@
+"""Host-side checks of the C ABI that need no GPU.
+
+* libepl.so loads and exports every function include/epl.h declares.
+* Argument errors are reported with the documented status BEFORE any HIP call. The pointers
+  below are fake addresses that the library must never dereference or launch on.
+* Workspace sizing follows the documented chunking.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_06202_amd import epl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "epl.h")
+
+OK, INVALID, ALIGN, CAPACITY, WORKSPACE, UNSUPPORTED = 0, 1, 2, 3, 4, 5
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(epl.LIB_PATH):
+        from paper_2607_06202_amd import _build
+        _build.build()
+    return epl.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(epl_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"epl_layout", "epl_dispatch", "epl_combine", "epl_workspace_bytes", "epl_status_str",
+            "epl_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), "libepl.so does not export " + n
+
+
+def test_version_and_status_strings(lib):
+    assert "gfx950" in epl.version()
+    for code in range(7):
+        s = lib.epl_status_str(code).decode()
+        assert s.startswith(epl.STATUS[code])
+
+
+class Fake:
+    """Distinct, 256-byte aligned fake device addresses (never dereferenced)."""
+    base = 0x7F0000000000
+
+    @classmethod
+    def ptr(cls, i, misalign=0):
+        return cls.base + 0x100000 * (i + 1) + misalign
+
+
+def fake_layout(misalign_field=None, null_field=None):
+    vals = []
+    for i, (n, _) in enumerate(epl.LayoutBuffers._fields_):
+        p = Fake.ptr(i, 2 if n == misalign_field else 0)
+        vals.append(None if n == null_field else p)
+    return epl.LayoutBuffers(*vals)
+
+
+def call_layout(lib, cfg, idx=Fake.ptr(50), L=None, ws=Fake.ptr(60), ws_bytes=1 << 30):
+    L = L if L is not None else fake_layout()
+    return lib.epl_layout(ctypes.byref(cfg), idx, ctypes.byref(L), ws, ws_bytes, None)
+
+
+GOOD = dict(R=8, E=64, k=8, H=7168, Tr=16)
+
+
+def cfg(**kw):
+    a = dict(GOOD)
+    a.update(kw)
+    return epl.config(a["R"], a["E"], a["k"], a["H"], a["Tr"], a.get("payload", "bf16"))
+
+
+@pytest.mark.parametrize("bad", [dict(R=0), dict(E=7), dict(E=4), dict(k=0), dict(k=33), dict(E=2048, R=8),
+                                 dict(H=7), dict(H=0), dict(Tr=-1), dict(R=64, E=256, k=32, Tr=1 << 21)])
+def test_layout_rejects_bad_config(lib, bad):
+    assert call_layout(lib, cfg(**bad)) == INVALID
+    assert lib.epl_workspace_bytes(ctypes.byref(cfg(**bad))) == 0
+
+
+def test_unknown_payload(lib):
+    c = cfg()
+    c.payload = 7
+    assert call_layout(lib, c) == UNSUPPORTED
+
+
+def test_layout_buffer_errors(lib):
+    assert lib.epl_layout(ctypes.byref(cfg()), Fake.ptr(50), None, Fake.ptr(60), 1 << 30, None) == INVALID
+    for n, _ in epl.LayoutBuffers._fields_:
+        assert call_layout(lib, cfg(), L=fake_layout(null_field=n)) == INVALID, n
+        assert call_layout(lib, cfg(), L=fake_layout(misalign_field=n)) == ALIGN, n
+    assert call_layout(lib, cfg(), idx=None) == INVALID
+    assert call_layout(lib, cfg(), idx=Fake.ptr(50, 1)) == ALIGN
+    assert call_layout(lib, cfg(), ws=None) == WORKSPACE
+    assert call_layout(lib, cfg(), ws=Fake.ptr(60, 2)) == ALIGN
+    need = lib.epl_workspace_bytes(ctypes.byref(cfg()))
+    assert call_layout(lib, cfg(), ws_bytes=need - 1) == WORKSPACE
+
+
+def test_workspace_formula(lib):
+    # chunks hold whole tokens, at most 1024 pairs: k=8 -> 128 tokens per chunk
+    for (R, E, k, Tr) in [(64, 256, 8, 128), (32, 256, 8, 4096), (256, 256, 8, 64), (4, 16, 2, 128), (3, 9, 5, 0),
+                          (2, 8, 1, 2500)]:
+        CT = max(1, min(Tr, 1024 // k)) if Tr > 0 else 1
+        NC = max(1, -(-Tr // CT)) if Tr > 0 else 1
+        nblk = R * NC
+        want = 4 * (E * nblk + nblk * R + E + nblk)
+        assert lib.epl_workspace_bytes(ctypes.byref(epl.config(R, E, k, 64, Tr))) == want
+
+
+def test_dispatch_errors(lib):
+    L = fake_layout()
+    x, recv, sc = Fake.ptr(70), Fake.ptr(71), Fake.ptr(72)
+    c = cfg()
+    cap = 8 * 16 * 8
+    d = lambda c, x=x, recv=recv, sc=sc, cap=cap, L=L: lib.epl_dispatch(ctypes.byref(c), x, ctypes.byref(L), recv, sc,
+                                                                        cap, None)
+    assert d(c, cap=cap - 1) == CAPACITY
+    assert d(c, x=Fake.ptr(70, 8)) == ALIGN
+    assert d(c, recv=Fake.ptr(71, 4)) == ALIGN
+    assert d(c, x=None) == INVALID
+    assert d(c, L=fake_layout(null_field="pair_row")) == INVALID
+    f8 = cfg(payload="fp8", H=7168 + 64)
+    assert d(f8) == UNSUPPORTED
+    f8 = cfg(payload="fp8")
+    assert d(f8, sc=None) == INVALID
+    assert d(f8, sc=Fake.ptr(72, 2)) == ALIGN
+
+
+def test_combine_errors(lib):
+    L = fake_layout()
+    c = cfg()
+    y, w, out = Fake.ptr(80), Fake.ptr(81), Fake.ptr(82)
+    cb = lambda y=y, w=w, out=out: lib.epl_combine(ctypes.byref(c), y, w, ctypes.byref(L), out, None)
+    assert cb(out=Fake.ptr(82, 8)) == ALIGN
+    assert cb(y=Fake.ptr(80, 2)) == ALIGN
+    assert cb(w=Fake.ptr(81, 2)) == ALIGN
+    assert cb(w=None) == INVALID
+
+
+def test_debug_errors(lib):
+    assert lib.epl_debug_f32_to_e4m3(Fake.ptr(1), Fake.ptr(2), -1, None) == INVALID
+    assert lib.epl_debug_f32_to_bf16(None, Fake.ptr(2), 5, None) == INVALID
+    assert lib.epl_debug_f32_to_bf16(Fake.ptr(1, 2), Fake.ptr(2), 5, None) == ALIGN
