@@ -70,6 +70,57 @@ def load_traffic(kernel, workload):
     return ent.get("bytes_per_launch")
 
 
+def _counter_means(csv_path):
+    """Mean counter value (KiB) per kernel name from a rocprofv3 --pmc counter_collection.csv."""
+    import csv
+    from collections import defaultdict
+
+    vals = defaultdict(list)
+    for r in csv.DictReader(open(csv_path)):
+        name = r["Kernel_Name"].split("(")[0].replace("void ", "").strip()
+        vals[name].append(float(r["Counter_Value"]))
+    return vals
+
+
+def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload, command):
+    """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE over this bench, and over
+    --calibrate-copy) into profiles/hbm_traffic.json and a text summary. The copy moves exactly
+    2^30 bytes each way, so bytes/counter for it calibrates the kernels' readings."""
+    n = float(1 << 30)
+    cf = _counter_means(copy_fetch_csv)["__amd_rocclr_copyBuffer"]
+    cw = _counter_means(copy_write_csv)["__amd_rocclr_copyBuffer"]
+    fetch_factor = n / (float(np.median(cf)) * 1024)
+    write_factor = n / (float(np.median(cw)) * 1024)
+    fetch = _counter_means(fetch_csv)
+    write = _counter_means(write_csv)
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        rec = {"kernels": {}}
+    rec["calibration"] = {"fetch_factor": round(fetch_factor, 4), "write_factor": round(write_factor, 4),
+                          "copy_bytes_each_way": int(n), "copy_fetch_kib": float(np.median(cf)),
+                          "copy_write_kib": float(np.median(cw))}
+    lines = ["HBM traffic per launch, workload %s (rocprofv3 FETCH_SIZE / WRITE_SIZE, KiB per dispatch)" % workload,
+             "commands:", *["  " + c for c in command],
+             "calibration: 1 GiB device copy reads FETCH_SIZE %.1f KiB (factor %.4f), WRITE_SIZE %.1f KiB (factor %.4f)"
+             % (np.median(cf), fetch_factor, np.median(cw), write_factor),
+             "%-40s %8s %14s %14s %16s" % ("kernel", "launches", "FETCH KiB", "WRITE KiB", "HBM bytes (cal.)")]
+    for name in fetch:
+        if not name.startswith("epl::"):
+            continue
+        short = name.split("::")[1].split("<")[0]
+        fk, wk = float(np.mean(fetch[name])), float(np.mean(write.get(name, [0.0])))
+        b = fk * 1024 * fetch_factor + wk * 1024 * write_factor
+        rec["kernels"]["%s@%s" % (short, workload)] = {"source_hash": source_hash(), "fetch_kib": fk,
+                                                        "write_kib": wk, "bytes_per_launch": int(round(b))}
+        lines.append("%-40s %8d %14.1f %14.1f %16d" % (name, len(fetch[name]), fk, wk, b))
+    lines.append("source hash of paper_2607_06202_amd/csrc: %s" % source_hash())
+    json.dump(rec, open(TRAFFIC_FILE, "w"), indent=1, sort_keys=True)
+    txt = os.path.join(ROOT, "profiles", "hbm_counters_%s.txt" % workload)
+    open(txt, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def cpu_baseline(w, idx, x, gw, budget_s):
     """The oracle (plain single-threaded C), timed on this host's CPU on the same inputs."""
     import oracle
@@ -103,7 +154,13 @@ def main():
     ap.add_argument("--cold-steps", type=int, default=30, help="extra cold-cache steps (0 to skip)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time (0 to skip)")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
+    ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="write profiles/hbm_traffic.json from rocprofv3 --pmc runs (no GPU needed)")
+    ap.add_argument("--command", action="append", default=[], help="profiler command recorded with --ingest-counters")
     args = ap.parse_args()
+    if args.ingest_counters:
+        ingest_counters(*args.ingest_counters, args.workload, args.command)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
