@@ -49,6 +49,7 @@ extern "C" {
 
 #define EPL_MAX_EXPERTS 1024 /* E (and therefore R) upper bound                        */
 #define EPL_MAX_TOPK 32      /* k upper bound                                            */
+#define EPL_MAX_HIDDEN 1048576 /* H upper bound (a row stays below 2^31 bytes)           */
 
 typedef enum {
   EPL_OK = 0,
@@ -66,7 +67,7 @@ typedef struct {
   int32_t num_ranks;       /* R >= 1                                                     */
   int32_t num_experts;     /* E, R <= E <= EPL_MAX_EXPERTS, E % R == 0                   */
   int32_t topk;            /* k, 1..EPL_MAX_TOPK                                         */
-  int32_t hidden;          /* H >= 8, H % 8 == 0 (bf16); H % 128 == 0 for fp8 dispatch   */
+  int32_t hidden;          /* 8 <= H <= EPL_MAX_HIDDEN, H % 8 == 0; H % 128 == 0 for fp8 */
   int32_t tokens_per_rank; /* Tr >= 0; T*k < 2^31                                        */
   int32_t payload;         /* epl_payload: dispatch output format                        */
 } epl_config;

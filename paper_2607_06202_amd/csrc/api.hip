@@ -21,7 +21,7 @@ epl_status check_config(const epl_config* cfg) {
   if (!cfg) return EPL_ERR_INVALID_ARG;
   const int R = cfg->num_ranks, E = cfg->num_experts, k = cfg->topk, H = cfg->hidden, Tr = cfg->tokens_per_rank;
   if (R < 1 || E < R || E > EPL_MAX_EXPERTS || E % R != 0) return EPL_ERR_INVALID_ARG;
-  if (k < 1 || k > EPL_MAX_TOPK || Tr < 0 || H < 8 || H % 8 != 0) return EPL_ERR_INVALID_ARG;
+  if (k < 1 || k > EPL_MAX_TOPK || Tr < 0 || H < 8 || H > EPL_MAX_HIDDEN || H % 8 != 0) return EPL_ERR_INVALID_ARG;
   if ((int64_t)R * Tr * k >= (int64_t)INT_MAX) return EPL_ERR_INVALID_ARG;
   if (cfg->payload != EPL_PAYLOAD_BF16 && cfg->payload != EPL_PAYLOAD_FP8_E4M3) return EPL_ERR_UNSUPPORTED;
   return EPL_OK;
@@ -37,12 +37,19 @@ epl::Geom make_geom(const epl_config* cfg) {
   g.k = cfg->topk;
   g.Tr = cfg->tokens_per_rank;
   g.T = (int64_t)g.R * g.Tr;
+  // Aim for >= 256 workgroups (the chip has 256 CUs) and >= 64 pairs per workgroup, with at
+  // most kMaxChunkPairs pairs per chunk.
   const int cap = epl::kMaxChunkPairs / g.k;  // k <= 32 so cap >= 32
-  g.CT = g.Tr < 1 ? 1 : (g.Tr < cap ? g.Tr : cap);
+  const int64_t want = std::max<int64_t>((g.T + 255) / 256, (64 + g.k - 1) / g.k);
+  const int ct = (int)std::min<int64_t>(want, cap);
+  g.CT = g.Tr < 1 ? 1 : std::min(ct, g.Tr);
   g.NC = g.Tr < 1 ? 1 : (g.Tr + g.CT - 1) / g.CT;
   g.nblk = g.R * g.NC;
   g.ebits = bits_for(g.E);
   g.rbits = bits_for(g.R);
+  g.inv_k = 1.0f / (float)g.k;
+  g.inv_El = 1.0f / (float)g.El;
+  g.inv_R = 1.0f / (float)g.R;
   return g;
 }
 

@@ -1,89 +1,91 @@
 // MoE combine on one GPU: gate-weighted gather-reduce of expert output rows back into token order
 // (the paper's combine: gather expert outputs and restore the original token order).
 //
-// One wave per token. The workgroup stages its tokens' k packed-row indices and k gate weights
-// in LDS with one coalesced load; each wave reads its own token's entries from there. The wave
-// then walks the row in passes of VPL 16-byte vectors per lane. Per pass it issues the loads of
-// up to KG expert rows before consuming any (many gathers in flight), then folds them in the
-// token's own j order, acc = fmaf(w_j, y_j, acc), in fp32 starting from +0. Results are rounded
-// to bf16 (RNE) and stored as 16-byte vectors. Pairs with row < 0 (invalid expert id) are
-// skipped.
+// Work is cut into equal units, each a (token, 1 KiB column chunk) pair, one unit per wave. The
+// workgroup stages its tokens' k packed-row indices and k gate weights in LDS with one coalesced
+// load. A wave issues the 16-byte loads of up to 8 expert rows before consuming any (many
+// gathers in flight). It then folds them in the token's own j order, acc = fmaf(w_j, y_j, acc),
+// in fp32 starting from +0, rounds to bf16 (RNE) and stores 16-byte vectors with nontemporal
+// stores (plain stores leave dirty lines whose write-back the next kernel pays for). Pairs with
+// row < 0 (invalid expert id) are skipped.
 #include "epl_internal.h"
 
 namespace epl {
 
 constexpr int kCombineThreads = 256;
-constexpr int kCombineTokens = kCombineThreads / kWave;
+constexpr int kCombineWaves = kCombineThreads / kWave;
+constexpr int kCombineCols = kWave;                  // one 16-byte vector per lane: 1 KiB of a row per unit
+constexpr int kGather = 8;                           // expert rows loaded before any is consumed
 
-template <int KG, int VPL>
+// One unit: gather chunk c of the token's k expert rows and fold them in j order. Row
+// indices and weights are wave-uniform and are read into scalar registers, so skipping an
+// invalid pair is a scalar branch. With k <= kGather all loads are issued before the first
+// fmaf. Larger k walks the choices in groups of kGather, still in j order.
+template <bool SMALL_K>
+__device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const int32_t* rows, const float* ws,
+                                             u32x4* __restrict__ out, int64_t g, int c, int k, int nv, int lane) {
+  const int v = c * kCombineCols + lane;
+  const bool on = v < nv;
+  const int vl = min(v, nv - 1);  // clamped so the gather loads need no per-lane branch
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+  const int kend = SMALL_K ? kGather : k;
+  for (int j0 = 0; j0 < kend; j0 += kGather) {
+    u32x4 buf[kGather];
+#pragma unroll
+    for (int jj = 0; jj < kGather; ++jj) {
+      const int j = j0 + jj;
+      const int row = j < k ? __builtin_amdgcn_readfirstlane(rows[j]) : -1;
+      if (row >= 0) buf[jj] = __builtin_nontemporal_load(y + (int64_t)row * nv + vl);
+    }
+#pragma unroll
+    for (int jj = 0; jj < kGather; ++jj) {
+      const int j = j0 + jj;
+      const int row = j < k ? __builtin_amdgcn_readfirstlane(rows[j]) : -1;
+      if (row < 0) continue;
+      const float wj = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, ws[j])));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] = fmaf(wj, bf16lo_to_f32(buf[jj][i]), acc[2 * i]);
+        acc[2 * i + 1] = fmaf(wj, bf16hi_to_f32(buf[jj][i]), acc[2 * i + 1]);
+      }
+    }
+  }
+  if (on) {
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = f32x2_to_bf16x2(acc[2 * i], acc[2 * i + 1]);
+    __builtin_nontemporal_store(o, out + g * nv + v);  // streamed: leaves no dirty lines behind
+  }
+}
+
+// unit = (token g, column chunk c). Units are numbered token-major, so one workgroup's waves
+// cover at most kCombineWaves consecutive tokens; their k row indices and k gate weights are
+// staged in LDS with one coalesced load per workgroup.
+template <bool SMALL_K>
 __global__ void __launch_bounds__(kCombineThreads)
     combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ w, const int32_t* __restrict__ pair_row,
-                   u32x4* __restrict__ out, int64_t T, int k, int nv) {
-  __shared__ int32_t rows_lds[kCombineTokens * EPL_MAX_TOPK];
-  __shared__ float w_lds[kCombineTokens * EPL_MAX_TOPK];
-  const int64_t g_first = (int64_t)blockIdx.x * kCombineTokens;
-  const int ntok = (int)min<int64_t>(kCombineTokens, T - g_first);
-  for (int i = threadIdx.x; i < ntok * k; i += kCombineThreads) {
-    rows_lds[i] = pair_row[g_first * k + i];
-    w_lds[i] = w[g_first * k + i];
-  }
-  __syncthreads();
-
+                   u32x4* __restrict__ out, int64_t T, int k, int nv, int chunks) {
+  __shared__ int32_t rows_lds[kCombineWaves * EPL_MAX_TOPK];
+  __shared__ float w_lds[kCombineWaves * EPL_MAX_TOPK];
+  const int64_t units = T * chunks;
   const int lane = threadIdx.x % kWave;
-  const int wv = threadIdx.x / kWave;
-  if (wv >= ntok) return;
-  const int64_t g = g_first + wv;
-  const int32_t* rows = rows_lds + wv * k;
-  const float* ws = w_lds + wv * k;
-
-  for (int v0 = 0; v0 < nv; v0 += kWave * VPL) {
-    float acc[VPL][8];
-#pragma unroll
-    for (int u = 0; u < VPL; ++u)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[u][e] = 0.0f;
-
-    for (int j0 = 0; j0 < k; j0 += KG) {
-      u32x4 buf[KG][VPL];
-#pragma unroll
-      for (int jj = 0; jj < KG; ++jj) {
-        const int j = j0 + jj;
-        const int row = (j < k) ? rows[j] : -1;
-        if (row < 0) continue;
-        const u32x4* src = y + (int64_t)row * nv;
-#pragma unroll
-        for (int u = 0; u < VPL; ++u) {
-          const int v = v0 + u * kWave + lane;
-          if (v < nv) buf[jj][u] = __builtin_nontemporal_load(src + v);
-        }
-      }
-#pragma unroll
-      for (int jj = 0; jj < KG; ++jj) {
-        const int j = j0 + jj;
-        if (j >= k) break;
-        const int row = rows[j];
-        if (row < 0) continue;
-        const float wj = ws[j];
-#pragma unroll
-        for (int u = 0; u < VPL; ++u) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            acc[u][2 * i] = fmaf(wj, bf16lo_to_f32(buf[jj][u][i]), acc[u][2 * i]);
-            acc[u][2 * i + 1] = fmaf(wj, bf16hi_to_f32(buf[jj][u][i]), acc[u][2 * i + 1]);
-          }
-        }
-      }
+  for (int64_t ub = (int64_t)blockIdx.x * kCombineWaves; ub < units; ub += (int64_t)gridDim.x * kCombineWaves) {
+    const int64_t g_first = ub / chunks;
+    const int64_t g_last = std::min(units - 1, ub + kCombineWaves - 1) / chunks;
+    const int ntok = (int)(g_last - g_first + 1);
+    __syncthreads();  // the previous iteration's readers are done with the staging buffers
+    for (int i = threadIdx.x; i < ntok * k; i += kCombineThreads) {
+      rows_lds[i] = pair_row[g_first * k + i];
+      w_lds[i] = w[g_first * k + i];
     }
-#pragma unroll
-    for (int u = 0; u < VPL; ++u) {
-      const int v = v0 + u * kWave + lane;
-      if (v < nv) {
-        u32x4 o;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = f32x2_to_bf16x2(acc[u][2 * i], acc[u][2 * i + 1]);
-        out[g * nv + v] = o;
-      }
-    }
+    __syncthreads();
+    const int64_t unit = ub + threadIdx.x / kWave;
+    if (unit >= units) continue;
+    const int64_t g = unit / chunks;
+    combine_unit<SMALL_K>(y, rows_lds + (g - g_first) * k, w_lds + (g - g_first) * k, out, g,
+                          (int)(unit - g * chunks), k, nv, lane);
   }
 }
 
@@ -91,10 +93,17 @@ hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row
                           int H, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const int nv = H / 8;
-  const dim3 grid((unsigned)((T + kCombineTokens - 1) / kCombineTokens));
+  const int chunks = (nv + kCombineCols - 1) / kCombineCols;
+  const int64_t blocks = (T * chunks + kCombineWaves - 1) / kCombineWaves;
+  const dim3 grid((unsigned)std::min<int64_t>(blocks, 1 << 30));
   const u32x4* yv = static_cast<const u32x4*>(y);
   u32x4* ov = static_cast<u32x4*>(out);
-  hipLaunchKernelGGL((combine_kernel<8, 2>), grid, dim3(kCombineThreads), 0, stream, yv, w, pair_row, ov, T, k, nv);
+  if (k <= kGather)
+    hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(kCombineThreads), 0, stream, yv, w, pair_row, ov, T, k, nv,
+                       chunks);
+  else
+    hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(kCombineThreads), 0, stream, yv, w, pair_row, ov, T, k, nv,
+                       chunks);
   return hipGetLastError();
 }
 

@@ -5,10 +5,11 @@
 // load/store; Background phase 2). Token-Reordering is fused in: the layout has already fixed
 // every row, so each copy lands in its final slot.
 //
-// One wave per token, and every token carries at most k rows, so a contiguous token range per
-// workgroup gives equal work per wave (the paper's equal token slices, Hierarchical Token-level
-// Scheduling). The token row is read once with 16-byte loads and written k times with 16-byte
-// nontemporal stores.
+// Work is cut into equal units, each a (token, column chunk) pair, one unit per wave. Every unit
+// moves at most k copies of the same number of bytes, so the units are as balanced as the
+// paper's equal token slices (Hierarchical Token-level Scheduling). Fine units also keep the
+// last partial round of waves short. The token's chunk is read once with 16-byte loads and
+// written k times with 16-byte stores.
 //
 // The fp8 variant quantises while copying. For each 128-element block the scale is
 // s = max|x| / 448, and each element is stored as q = E4M3(x / s), RNE and saturating. It
@@ -18,113 +19,116 @@
 namespace epl {
 
 constexpr int kDispatchThreads = 256;
-constexpr int kTokensPerBlock = kDispatchThreads / kWave;
+constexpr int kWavesPerBlock = kDispatchThreads / kWave;
+// bf16 work unit: one token's columns [u*kBf16Cols, (u+1)*kBf16Cols) in 16-byte vectors.
+constexpr int kBf16VPL = 4;                     // vectors per lane in one unit
+constexpr int kBf16Cols = kWave * kBf16VPL;     // 256 vectors = 4 KiB of a row
 
-// bf16: a row is nv = H/8 16-byte vectors; each lane holds up to VPL of them per pass.
-template <int VPL>
-__global__ void __launch_bounds__(kDispatchThreads)
-    dispatch_bf16_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
-                         int64_t T, int k, int nv, int64_t cap) {
-  const int lane = threadIdx.x % kWave;
-  const int64_t g = (int64_t)blockIdx.x * kTokensPerBlock + threadIdx.x / kWave;
-  if (g >= T) return;
+// Store one 16-byte vector at vector index v of a row of nv vectors through a buffer resource
+// scoped to that row, with an explicit cache policy. The resource bounds (nv * 16 bytes) also
+// guard the row. Measured on MI355X, layout -> dispatch -> combine back to back:
+// * bf16 rows: sc1 beat default-policy stores. Nontemporal stores were slower, because they
+//   make the dispatch pay its whole write cost before the next kernel can start.
+// * fp8 rows: sc1+nt beat both.
+template <int POLICY>
+__device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int nv, int v) {
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(row_base, 0, nv * 16, kBufferRsrcWord3);
+  __builtin_amdgcn_raw_buffer_store_b128(val, rsrc, v * 16, 0, POLICY);
+}
+
+// bf16: unit = (token g, column chunk c). The wave loads its chunk of x[g] once (nontemporal:
+// x is read exactly once) and stores it to the k destination rows, interleaving destinations
+// per vector.
+__device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row,
+                                                   u32x4* __restrict__ recv, int64_t g, int c, int k, int nv,
+                                                   int64_t cap, int lane) {
   const int my_row = lane < k ? pair_row[g * k + lane] : -1;
   const u32x4* xr = x + g * nv;
-  for (int v0 = 0; v0 < nv; v0 += kWave * VPL) {
-    u32x4 buf[VPL];
+  const int v0 = c * kBf16Cols + lane;
+  // Loads are unconditional (index clamped into the row) so that all of them are in flight
+  // together; only the stores are guarded.
+  u32x4 buf[kBf16VPL];
 #pragma unroll
-    for (int u = 0; u < VPL; ++u) {
-      const int v = v0 + u * kWave + lane;
-      if (v < nv) buf[u] = __builtin_nontemporal_load(xr + v);
-    }
+  for (int u = 0; u < kBf16VPL; ++u) buf[u] = __builtin_nontemporal_load(xr + min(v0 + u * kWave, nv - 1));
+#pragma unroll
+  for (int u = 0; u < kBf16VPL; ++u) {
+    const int v = v0 + u * kWave;
     for (int j = 0; j < k; ++j) {
       const int row = __builtin_amdgcn_readlane(my_row, j);
       if (row < 0 || row >= cap) continue;
-      u32x4* dst = recv + (int64_t)row * nv;
-#pragma unroll
-      for (int u = 0; u < VPL; ++u) {
-        const int v = v0 + u * kWave + lane;
-        if (v < nv) __builtin_nontemporal_store(buf[u], dst + v);
-      }
+      if (v < nv) store_row_policy<kCachePolicySc1>(buf[u], recv + (int64_t)row * nv, nv, v);
     }
   }
 }
 
-// fp8: a pass covers 1024 elements; lane l quantises elements [16l, 16l+16) of the pass (two
-// 16-byte bf16 loads -> one 16-byte E4M3 store). A 128-element block spans 8 lanes, whose
-// max is combined with three xor-shuffles. Up to PASSES passes are held in registers before
-// being stored to every destination; per-block scales go through LDS so that each
-// destination's scale row is stored with contiguous lanes.
-template <int PASSES>
 __global__ void __launch_bounds__(kDispatchThreads)
-    dispatch_fp8_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
-                        float* __restrict__ recv_scale, int64_t T, int k, int H, int64_t cap) {
-  extern __shared__ float sc_lds[];  // [kTokensPerBlock][NB]
+    dispatch_bf16_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
+                         int64_t T, int k, int nv, int chunks, int64_t cap) {
   const int lane = threadIdx.x % kWave;
-  const int wv = threadIdx.x / kWave;
-  const int64_t g = (int64_t)blockIdx.x * kTokensPerBlock + wv;
-  if (g >= T) return;
+  const int64_t units = T * chunks;
+  const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
+  for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
+    const int64_t g = u / chunks;
+    dispatch_bf16_unit(x, pair_row, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
+  }
+}
+
+// fp8: unit = (token g, pass p) covering elements [1024p, 1024p + 1024). Lane l quantises
+// elements [16l, 16l+16) of the pass: two 16-byte bf16 loads -> one 16-byte E4M3 store per
+// destination. A 128-element block spans 8 lanes, whose max is combined with three
+// xor-shuffles; the first lane of each block stores that block's scale for every destination.
+__device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row,
+                                                  u32x4* __restrict__ recv, float* __restrict__ recv_scale, int64_t g,
+                                                  int p, int k, int H, int64_t cap, int lane) {
   const int NB = H / 128;
-  float* sc = sc_lds + wv * NB;
+  const int nvq = H / 16;  // 16-byte fp8 vectors per row
   const int my_row = lane < k ? pair_row[g * k + lane] : -1;
   const u32x4* xr = x + g * (H / 8);
-  const int nvq = H / 16;  // 16-byte fp8 vectors per row
-  const int npass = (H + 1023) / 1024;
-
-  for (int p0 = 0; p0 < npass; p0 += PASSES) {
-    u32x4 q[PASSES];
+  const int vq = p * kWave + lane;  // fp8 vector index = element / 16
+  const bool on = vq < nvq;         // whole 8-lane blocks are on or off (H % 128 == 0)
+  const int vl = min(vq, nvq - 1);  // clamped so the loads need no branch
+  u32x4 a = __builtin_nontemporal_load(xr + 2 * vl);
+  u32x4 bv = __builtin_nontemporal_load(xr + 2 * vl + 1);
+  if (!on) a = bv = u32x4{0, 0, 0, 0};
+  float f[16];
 #pragma unroll
-    for (int pp = 0; pp < PASSES; ++pp) {
-      const int vq = (p0 + pp) * kWave + lane;  // fp8 vector index = element / 16
-      const bool on = (p0 + pp < npass) && (vq < nvq);
-      u32x4 a = {0, 0, 0, 0}, bv = {0, 0, 0, 0};
-      if (on) {
-        a = __builtin_nontemporal_load(xr + 2 * vq);
-        bv = __builtin_nontemporal_load(xr + 2 * vq + 1);
-      }
-      float f[16];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f[2 * i] = bf16lo_to_f32(a[i]);
-        f[2 * i + 1] = bf16hi_to_f32(a[i]);
-        f[8 + 2 * i] = bf16lo_to_f32(bv[i]);
-        f[8 + 2 * i + 1] = bf16hi_to_f32(bv[i]);
-      }
-      float amax = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(f[i]));
-      amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
-      amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
-      amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
-      const float s = amax / 448.0f;
-      u32x4 o = {0, 0, 0, 0};
-      if (amax != 0.0f) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          o[i] = f32x4_to_e4m3x4(f[4 * i] / s, f[4 * i + 1] / s, f[4 * i + 2] / s, f[4 * i + 3] / s);
-      }
-      q[pp] = o;
-      if (on && (lane % 8) == 0) sc[vq / 8] = s;
-    }
-    for (int j = 0; j < k; ++j) {
-      const int row = __builtin_amdgcn_readlane(my_row, j);
-      if (row < 0 || row >= cap) continue;
-      u32x4* dst = recv + (int64_t)row * nvq;
-#pragma unroll
-      for (int pp = 0; pp < PASSES; ++pp) {
-        const int vq = (p0 + pp) * kWave + lane;
-        if ((p0 + pp < npass) && (vq < nvq)) __builtin_nontemporal_store(q[pp], dst + vq);
-      }
-    }
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = bf16lo_to_f32(a[i]);
+    f[2 * i + 1] = bf16hi_to_f32(a[i]);
+    f[8 + 2 * i] = bf16lo_to_f32(bv[i]);
+    f[8 + 2 * i + 1] = bf16hi_to_f32(bv[i]);
   }
-  // Scales: the wave's own LDS writes are complete before these reads.
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(f[i]));
+  amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
+  amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
+  amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
+  const float s = amax / 448.0f;
+  u32x4 q = {0, 0, 0, 0};
+  if (amax != 0.0f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      q[i] = f32x4_to_e4m3x4(f[4 * i] / s, f[4 * i + 1] / s, f[4 * i + 2] / s, f[4 * i + 3] / s);
+  }
+  const bool scale_lane = on && (lane % 8) == 0;
   for (int j = 0; j < k; ++j) {
     const int row = __builtin_amdgcn_readlane(my_row, j);
     if (row < 0 || row >= cap) continue;
-    float* dst = recv_scale + (int64_t)row * NB;
-    for (int bk = lane; bk < NB; bk += kWave) __builtin_nontemporal_store(sc[bk], dst + bk);
+    if (on) store_row_policy<kCachePolicySc1Nt>(q, recv + (int64_t)row * nvq, nvq, vq);
+    if (scale_lane) __builtin_nontemporal_store(s, recv_scale + (int64_t)row * NB + vq / 8);
+  }
+}
+
+__global__ void __launch_bounds__(kDispatchThreads)
+    dispatch_fp8_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
+                        float* __restrict__ recv_scale, int64_t T, int k, int H, int npass, int64_t cap) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t units = T * npass;
+  const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
+  for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
+    const int64_t g = u / npass;
+    dispatch_fp8_unit(x, pair_row, recv, recv_scale, g, (int)(u - g * npass), k, H, cap, lane);
   }
 }
 
@@ -132,24 +136,22 @@ hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* re
                                 int64_t cap, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const int nv = H / 8;
-  const dim3 grid((unsigned)((T + kTokensPerBlock - 1) / kTokensPerBlock));
-  const u32x4* xv = static_cast<const u32x4*>(x);
-  u32x4* rv = static_cast<u32x4*>(recv);
-  if (nv <= kWave * 4)
-    hipLaunchKernelGGL(dispatch_bf16_kernel<4>, grid, dim3(kDispatchThreads), 0, stream, xv, pair_row, rv, T, k, nv, cap);
-  else
-    hipLaunchKernelGGL(dispatch_bf16_kernel<14>, grid, dim3(kDispatchThreads), 0, stream, xv, pair_row, rv, T, k,
-                       nv, cap);
+  const int chunks = (nv + kBf16Cols - 1) / kBf16Cols;
+  const int64_t units = T * chunks;
+  const dim3 grid((unsigned)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30));
+  hipLaunchKernelGGL(dispatch_bf16_kernel, grid, dim3(kDispatchThreads), 0, stream, static_cast<const u32x4*>(x),
+                     pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
   return hipGetLastError();
 }
 
 hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* recv, float* recv_scale, int64_t T,
                                int k, int H, int64_t cap, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  const dim3 grid((unsigned)((T + kTokensPerBlock - 1) / kTokensPerBlock));
-  const size_t lds = sizeof(float) * (size_t)kTokensPerBlock * (H / 128);
-  hipLaunchKernelGGL(dispatch_fp8_kernel<7>, grid, dim3(kDispatchThreads), lds, stream,
-                     static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), recv_scale, T, k, H, cap);
+  const int npass = (H + 1023) / 1024;
+  const int64_t units = T * npass;
+  const dim3 grid((unsigned)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30));
+  hipLaunchKernelGGL(dispatch_fp8_kernel, grid, dim3(kDispatchThreads), 0, stream, static_cast<const u32x4*>(x),
+                     pair_row, static_cast<u32x4*>(recv), recv_scale, T, k, H, npass, cap);
   return hipGetLastError();
 }
 

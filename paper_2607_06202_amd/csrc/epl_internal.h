@@ -2,6 +2,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -19,6 +21,12 @@ constexpr int kChunkSlots = kMaxChunkPairs / kLayoutThreads;  // register slots 
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Buffer resource descriptor word 3 for raw (untyped) buffer accesses on CDNA3/CDNA4.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+// Cache-policy operand of the raw buffer builtins: bit 0 = sc0, bit 1 = nt, bit 4 = sc1.
+constexpr int kCachePolicySc1 = 16;
+constexpr int kCachePolicySc1Nt = 18;
+
 // Shape of one layout problem, derived on the host from epl_config.
 struct Geom {
   int R, E, El, k, Tr;
@@ -27,6 +35,7 @@ struct Geom {
   int nblk;   // R * NC layout workgroups
   int ebits;  // bits needed for an expert id (ballot-match key width)
   int rbits;  // bits needed for a rank id
+  float inv_k, inv_El, inv_R;  // 1/k, 1/El, 1/R for exact small quotients
   int64_t T;
 };
 
@@ -36,6 +45,8 @@ struct WsLayout {
   size_t chunk_r;   // [nblk][R]  per-chunk first-pair counts per destination rank, then slot bases
   size_t recv_cnt;  // [E]
   size_t inval;     // [nblk]
+  size_t seg_rel;   // [E][R]     segment offsets relative to the expert start
+  size_t fmask;     // [T]        per-token bitmask of first pairs per destination rank
   size_t total;
 };
 
@@ -50,6 +61,10 @@ inline WsLayout ws_layout(const Geom& g) {
   o += (size_t)g.E;
   w.inval = o;
   o += (size_t)g.nblk;
+  w.seg_rel = o;
+  o += (size_t)g.E * g.R;
+  w.fmask = o;
+  o += (size_t)g.T;
   w.total = o;
   return w;
 }

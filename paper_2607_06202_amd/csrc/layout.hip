@@ -9,27 +9,35 @@
 //
 // Three launches, no atomics that decide an order, bit-identical on every run:
 //   K1 route_hist      one workgroup per chunk (CT whole tokens of one source rank): LDS
-//                      histograms of expert ids and of first-per-token destination ranks,
-//                      tok_nranks, invalid count.
+//                      histograms of expert ids and of first-per-token destination ranks, the
+//                      per-token first-pair bitmask, tok_nranks and the invalid count.
 //   K2 route_scan      one workgroup per expert column: scan over (source rank, chunk) giving
-//                      seg_off (relative to the expert start), send_cnt, recv_cnt and per-chunk
-//                      base rows. One workgroup per source rank: scan of rank slots over chunks.
-//                      One workgroup: num_invalid.
+//                      segment offsets relative to the expert start, send_cnt, recv_cnt and
+//                      per-chunk base rows. One workgroup per source rank: scan of rank slots
+//                      over chunks. One workgroup: num_invalid.
 //   K3 route_finalize  one workgroup per chunk: expert_off via an LDS scan of recv_cnt. Each
 //                      wave takes a contiguous quarter of the chunk's pairs and gives every pair
 //                      its stable rank among equal keys: ballot match over the key bits,
 //                      popcount of the lanes below, per-wave LDS running counts. A cross-wave
 //                      prefix then yields pair_row, recv_src, recv_j and pair_rslot.
+//
+// Small integer quotients (pair -> token, expert -> rank, both numerators < 2^21) use
+// q = (int)((n + 0.5f) * (1.0f / d)). The exact quotient sits at least 0.5/d away from an
+// integer, and two float roundings perturb (n + 0.5)/d by at most (n + 0.5) * 2^-22 / d, which is
+// smaller than 0.5/d. So the truncated result is exact.
 #include "epl_internal.h"
 
 namespace epl {
 
+__device__ __forceinline__ int small_div(int n, float inv_d) { return (int)(((float)n + 0.5f) * inv_d); }
+
 // ------------------------------------------------------------------------------------ K1
 __global__ void __launch_bounds__(kLayoutThreads)
     route_hist_kernel(Geom G, const int32_t* __restrict__ idx, int32_t* __restrict__ tok_nranks,
-                      int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r, int32_t* __restrict__ inval) {
+                      int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r, int32_t* __restrict__ inval,
+                      uint32_t* __restrict__ fmask) {
   extern __shared__ int32_t lds[];
-  int32_t* hist_e = lds;          // [E]
+  int32_t* hist_e = lds;           // [E]
   int32_t* hist_r = hist_e + G.E;  // [R]
   int32_t* dst = hist_r + G.R;     // [kMaxChunkPairs] destination rank of each pair, -1 if invalid
   __shared__ int32_t red[kLayoutWaves];
@@ -51,7 +59,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
   for (int i = tid; i < np; i += kLayoutThreads) {
     const int e = src[i];
     const bool ok = (unsigned)e < (unsigned)G.E;
-    dst[i] = ok ? e / G.El : -1;
+    dst[i] = ok ? small_div(e, G.inv_El) : -1;
     if (ok)
       atomicAdd(&hist_e[e], 1);
     else
@@ -63,7 +71,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
   // of the token targets the same rank. One thread per token.
   for (int t = tid; t < nt; t += kLayoutThreads) {
     const int32_t* dt = dst + t * G.k;
-    int nr = 0;
+    uint32_t mask = 0;
     for (int j = 0; j < G.k; ++j) {
       const int d = dt[j];
       if (d < 0) continue;
@@ -71,10 +79,11 @@ __global__ void __launch_bounds__(kLayoutThreads)
       for (int jj = 0; jj < j; ++jj) first &= (dt[jj] != d);
       if (first) {
         atomicAdd(&hist_r[d], 1);
-        ++nr;
+        mask |= 1u << j;
       }
     }
-    tok_nranks[g0 + t] = nr;
+    tok_nranks[g0 + t] = __popc(mask);
+    fmask[g0 + t] = mask;
   }
 
   const int wsum = wave_sum(my_inval);
@@ -94,7 +103,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
 __global__ void __launch_bounds__(kLayoutThreads)
     route_scan_kernel(Geom G, int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r,
                       const int32_t* __restrict__ inval, int32_t* __restrict__ recv_cnt, int32_t* __restrict__ send_cnt,
-                      int32_t* __restrict__ rank_cnt, int32_t* __restrict__ seg_off, int32_t* __restrict__ num_invalid) {
+                      int32_t* __restrict__ rank_cnt, int32_t* __restrict__ seg_rel, int32_t* __restrict__ num_invalid) {
   __shared__ int32_t scratch[kLayoutWaves];
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
@@ -112,8 +121,8 @@ __global__ void __launch_bounds__(kLayoutThreads)
       const int excl = block_exclusive_sum(sum, total, scratch);
       if (s < G.R) {
         const int base = carry + excl;
-        seg_off[(int64_t)e * G.R + s] = base;  // K3 adds expert_off[e]
-        send_cnt[(int64_t)s * G.E + e] = sum;
+        seg_rel[e * G.R + s] = base;
+        send_cnt[s * G.E + e] = sum;
         int run = base;
         for (int c = 0; c < G.NC; ++c) {
           const int h = col[s * G.NC + c];
@@ -135,7 +144,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
         *p = run;
         run += h;
       }
-      rank_cnt[(int64_t)s * G.R + r] = run;
+      rank_cnt[s * G.R + r] = run;
     }
   } else {
     int n = 0;
@@ -155,18 +164,20 @@ __global__ void __launch_bounds__(kLayoutThreads)
 __global__ void __launch_bounds__(kLayoutThreads)
     route_finalize_kernel(Geom G, const int32_t* __restrict__ idx, const int32_t* __restrict__ chunk_e,
                           const int32_t* __restrict__ chunk_r, const int32_t* __restrict__ recv_cnt,
+                          const int32_t* __restrict__ seg_rel, const uint32_t* __restrict__ fmask,
                           int32_t* __restrict__ expert_off, int32_t* __restrict__ rank_off, int32_t* __restrict__ seg_off,
                           int32_t* __restrict__ pair_row, int32_t* __restrict__ pair_rslot, int32_t* __restrict__ recv_src,
                           int32_t* __restrict__ recv_j) {
   extern __shared__ int32_t lds[];
-  int32_t* eoff = lds;                               // [E+1]
-  int32_t* base_e = eoff + G.E + 1;                  // [E]   first packed row of this chunk's pairs of expert e
-  int32_t* base_r = base_e + G.E;                    // [R]   first slot of this chunk's tokens bound for rank r
-  int32_t* whe = base_r + G.R;                       // [W][E] per-wave counts, then per-wave bases
-  int32_t* whr = whe + kLayoutWaves * G.E;           // [W][R]
-  int32_t* ekey = whr + kLayoutWaves * G.R;          // [kMaxChunkPairs] expert id, -1 invalid
-  int32_t* dkey = ekey + kMaxChunkPairs;             // [kMaxChunkPairs] destination rank, -1 invalid
-  int32_t* rs = dkey + kMaxChunkPairs;               // [kMaxChunkPairs] slot of first pairs
+  int32_t* eoff = lds;                       // [E+1]
+  int32_t* base_e = eoff + G.E + 1;          // [E]   first packed row of this chunk's pairs of expert e
+  int32_t* base_r = base_e + G.E;            // [R]   first slot of this chunk's tokens bound for rank r
+  int32_t* whe = base_r + G.R;               // [W][E] per-wave counts, then per-wave bases
+  int32_t* whr = whe + kLayoutWaves * G.E;   // [W][R]
+  int32_t* ekey = whr + kLayoutWaves * G.R;  // [kMaxChunkPairs] expert id, -1 invalid
+  int32_t* dkey = ekey + kMaxChunkPairs;     // [kMaxChunkPairs] destination rank, -1 invalid
+  int32_t* rs = dkey + kMaxChunkPairs;       // [kMaxChunkPairs] slot of first pairs
+  uint32_t* fm = reinterpret_cast<uint32_t*>(rs + kMaxChunkPairs);  // [kMaxChunkPairs / 1] token masks
   __shared__ int32_t scratch[kLayoutWaves];
 
   const int tid = threadIdx.x;
@@ -178,13 +189,17 @@ __global__ void __launch_bounds__(kLayoutThreads)
   const int np = nt * G.k;
   const int64_t g0 = (int64_t)s * G.Tr + t0;
 
+  // All global inputs of this workgroup are independent: issue them together.
   const int32_t* src = idx + g0 * G.k;
   for (int i = tid; i < np; i += kLayoutThreads) {
     const int e = src[i];
     const bool ok = (unsigned)e < (unsigned)G.E;
     ekey[i] = ok ? e : -1;
-    dkey[i] = ok ? e / G.El : -1;
+    dkey[i] = ok ? small_div(e, G.inv_El) : -1;
   }
+  for (int t = tid; t < nt; t += kLayoutThreads) fm[t] = fmask[g0 + t];
+  for (int e = tid; e < G.E; e += kLayoutThreads) base_e[e] = chunk_e[(int64_t)e * G.nblk + b];
+  for (int r = tid; r < G.R; r += kLayoutThreads) base_r[r] = chunk_r[(int64_t)b * G.R + r];
   for (int i = tid; i < kLayoutWaves * (G.E + G.R); i += kLayoutThreads) whe[i] = 0;
 
   // expert_off = exclusive scan of recv_cnt; each thread owns a contiguous run of experts.
@@ -194,27 +209,13 @@ __global__ void __launch_bounds__(kLayoutThreads)
     int sum = 0;
     for (int e = e0; e < e1; ++e) sum += recv_cnt[e];
     int total;
-    int run = block_exclusive_sum(sum, total, scratch);
+    int run = block_exclusive_sum(sum, total, scratch);  // synchronises the workgroup
     for (int e = e0; e < e1; ++e) {
       eoff[e] = run;
+      base_e[e] += run;
       run += recv_cnt[e];
     }
     if (tid == 0) eoff[G.E] = total;
-  }
-  __syncthreads();
-
-  for (int e = tid; e < G.E; e += kLayoutThreads) base_e[e] = eoff[e] + chunk_e[(int64_t)e * G.nblk + b];
-  for (int r = tid; r < G.R; r += kLayoutThreads) base_r[r] = chunk_r[(int64_t)b * G.R + r];
-  if (b == 0) {
-    for (int e = tid; e <= G.E; e += kLayoutThreads) expert_off[e] = eoff[e];
-    for (int d = tid; d <= G.R; d += kLayoutThreads) rank_off[d] = eoff[d * G.El];
-  }
-  {
-    // seg_off holds offsets relative to the expert start; each workgroup rebases one slice.
-    const int64_t n = (int64_t)G.E * G.R;
-    const int64_t per = (n + G.nblk - 1) / G.nblk;
-    const int64_t i0 = (int64_t)b * per, i1 = min(n, i0 + per);
-    for (int64_t i = i0 + tid; i < i1; i += kLayoutThreads) seg_off[i] += eoff[i / G.R];
   }
   __syncthreads();
 
@@ -226,7 +227,6 @@ __global__ void __launch_bounds__(kLayoutThreads)
   const int p_beg = w * Q;
   const int p_end = min(np, p_beg + Q);
   int rank_e[kChunkSlots], rank_r[kChunkSlots];
-  uint32_t first_bits = 0;
 #pragma unroll
   for (int it = 0; it < kChunkSlots; ++it) {
     rank_e[it] = 0;
@@ -237,26 +237,19 @@ __global__ void __launch_bounds__(kLayoutThreads)
     const int e = active ? ekey[p] : -1;
     const int d = active ? dkey[p] : -1;
     const bool valid = e >= 0;
-    bool first = valid;
-    if (valid) {
-      const int t = p / G.k;
-      const int j = p - t * G.k;
-      for (int jj = 0; jj < j; ++jj) first &= (dkey[t * G.k + jj] != d);
-    }
-    first_bits |= first ? (1u << it) : 0u;
+    const int t = small_div(p, G.inv_k);
+    const bool first = valid && ((fm[t] >> (p - t * G.k)) & 1u);
 
     const uint64_t me = match_key(valid, e, G.ebits);
     const int lo_e = rank_in_mask(me);
-    const int cnt_e = __popcll(me);
     const int seen_e = valid ? whe[w * G.E + e] : 0;
-    if (valid && lo_e == 0) whe[w * G.E + e] = seen_e + cnt_e;  // one lane per key
+    if (valid && lo_e == 0) whe[w * G.E + e] = seen_e + __popcll(me);  // one lane per key
     rank_e[it] = seen_e + lo_e;
 
     const uint64_t mr = match_key(first, d, G.rbits);
     const int lo_r = rank_in_mask(mr);
-    const int cnt_r = __popcll(mr);
     const int seen_r = first ? whr[w * G.R + d] : 0;
-    if (first && lo_r == 0) whr[w * G.R + d] = seen_r + cnt_r;
+    if (first && lo_r == 0) whr[w * G.R + d] = seen_r + __popcll(mr);
     rank_r[it] = seen_r + lo_r;
   }
   __syncthreads();
@@ -282,28 +275,29 @@ __global__ void __launch_bounds__(kLayoutThreads)
   }
   __syncthreads();
 
+  const int P = eoff[G.E];
 #pragma unroll
   for (int it = 0; it < kChunkSlots; ++it) {
     if (p_beg + it * kWave >= p_end) continue;
     const int p = p_beg + it * kWave + lane;
     if (p >= p_end) continue;
     const int e = ekey[p];
-    const int t = p / G.k;
+    const int t = small_div(p, G.inv_k);
     const int j = p - t * G.k;
     const int64_t g = g0 + t;
     if (e >= 0) {
       const int row = base_e[e] + whe[w * G.E + e] + rank_e[it];
       pair_row[g * G.k + j] = row;
-      if (row < eoff[G.E]) {  // always true for a consistent layout; keeps stores in bounds
+      if (row < P) {  // always true for a consistent layout; keeps stores in bounds
         recv_src[row] = (int32_t)g;
         recv_j[row] = j;
       }
+      if ((fm[t] >> j) & 1u) {
+        const int d = dkey[p];
+        rs[p] = base_r[d] + whr[w * G.R + d] + rank_r[it];
+      }
     } else {
       pair_row[g * G.k + j] = -1;
-    }
-    if (first_bits & (1u << it)) {
-      const int d = dkey[p];
-      rs[p] = base_r[d] + whr[w * G.R + d] + rank_r[it];
     }
   }
   __syncthreads();
@@ -311,7 +305,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
   // Every valid pair reports the slot of its token's first pair on the same rank.
   for (int p = tid; p < np; p += kLayoutThreads) {
     const int d = dkey[p];
-    const int t = p / G.k;
+    const int t = small_div(p, G.inv_k);
     int slot = -1;
     if (d >= 0) {
       int jf = t * G.k;
@@ -320,11 +314,22 @@ __global__ void __launch_bounds__(kLayoutThreads)
     }
     pair_rslot[(g0 + t) * G.k + (p - t * G.k)] = slot;
   }
+
+  // Global offsets, off the critical path: block 0 writes expert_off and rank_off; every
+  // workgroup rebases one slice of the (expert, source) segment offsets.
+  if (b == 0) {
+    for (int e = tid; e <= G.E; e += kLayoutThreads) expert_off[e] = eoff[e];
+    for (int d = tid; d <= G.R; d += kLayoutThreads) rank_off[d] = eoff[d * G.El];
+  }
+  const int n = G.E * G.R;
+  const int per = (n + G.nblk - 1) / G.nblk;
+  const int i1 = min(n, (b + 1) * per);
+  for (int i = b * per + tid; i < i1; i += kLayoutThreads) seg_off[i] = eoff[small_div(i, G.inv_R)] + seg_rel[i];
 }
 
 // ------------------------------------------------------------------------------------ host
 static size_t finalize_lds_bytes(const Geom& g) {
-  return sizeof(int32_t) * ((size_t)(g.E + 1) + g.E + g.R + (size_t)kLayoutWaves * (g.E + g.R) + 3 * kMaxChunkPairs);
+  return sizeof(int32_t) * ((size_t)(g.E + 1) + g.E + g.R + (size_t)kLayoutWaves * (g.E + g.R) + 4 * kMaxChunkPairs);
 }
 
 hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
@@ -336,21 +341,23 @@ hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t
   int32_t* chunk_r = ws + wl.chunk_r;
   int32_t* recv_cnt = ws + wl.recv_cnt;
   int32_t* inval = ws + wl.inval;
+  int32_t* seg_rel = ws + wl.seg_rel;
+  uint32_t* fmask = reinterpret_cast<uint32_t*>(ws + wl.fmask);
 
   const size_t lds1 = sizeof(int32_t) * ((size_t)g.E + g.R + kMaxChunkPairs);
   hipLaunchKernelGGL(route_hist_kernel, dim3(g.nblk), dim3(kLayoutThreads), lds1, stream, g, idx, tok_nranks,
-                     chunk_e, chunk_r, inval);
+                     chunk_e, chunk_r, inval, fmask);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
 
   hipLaunchKernelGGL(route_scan_kernel, dim3(g.E + g.R + 1), dim3(kLayoutThreads), 0, stream, g, chunk_e, chunk_r,
-                     inval, recv_cnt, send_cnt, rank_cnt, seg_off, num_invalid);
+                     inval, recv_cnt, send_cnt, rank_cnt, seg_rel, num_invalid);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
 
   hipLaunchKernelGGL(route_finalize_kernel, dim3(g.nblk), dim3(kLayoutThreads), finalize_lds_bytes(g), stream, g,
-                     idx, chunk_e, chunk_r, recv_cnt, expert_off, rank_off, seg_off, pair_row, pair_rslot, recv_src,
-                     recv_j);
+                     idx, chunk_e, chunk_r, recv_cnt, seg_rel, fmask, expert_off, rank_off, seg_off, pair_row,
+                     pair_rslot, recv_src, recv_j);
   return hipGetLastError();
 }
 

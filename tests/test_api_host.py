@@ -80,7 +80,7 @@ def cfg(**kw):
 
 
 @pytest.mark.parametrize("bad", [dict(R=0), dict(E=7), dict(E=4), dict(k=0), dict(k=33), dict(E=2048, R=8),
-                                 dict(H=7), dict(H=0), dict(Tr=-1), dict(R=64, E=256, k=32, Tr=1 << 21)])
+                                 dict(H=7), dict(H=0), dict(H=1 << 21), dict(Tr=-1), dict(R=64, E=256, k=32, Tr=1 << 21)])
 def test_layout_rejects_bad_config(lib, bad):
     assert call_layout(lib, cfg(**bad)) == INVALID
     assert lib.epl_workspace_bytes(ctypes.byref(cfg(**bad))) == 0
@@ -106,14 +106,17 @@ def test_layout_buffer_errors(lib):
 
 
 def test_workspace_formula(lib):
-    # chunks hold whole tokens, at most 1024 pairs: k=8 -> 128 tokens per chunk
+    # Chunks hold whole tokens. There are at most 1024 pairs per chunk. The target is >= 256
+    # workgroups and >= 64 pairs per workgroup.
     for (R, E, k, Tr) in [(64, 256, 8, 128), (32, 256, 8, 4096), (256, 256, 8, 64), (4, 16, 2, 128), (3, 9, 5, 0),
-                          (2, 8, 1, 2500)]:
-        CT = max(1, min(Tr, 1024 // k)) if Tr > 0 else 1
-        NC = max(1, -(-Tr // CT)) if Tr > 0 else 1
+                          (2, 8, 1, 2500), (1024, 1024, 32, 3)]:
+        T = R * Tr
+        want = max(-(-T // 256), -(-64 // k))
+        CT = min(min(want, 1024 // k), Tr) if Tr > 0 else 1
+        NC = -(-Tr // CT) if Tr > 0 else 1
         nblk = R * NC
-        want = 4 * (E * nblk + nblk * R + E + nblk)
-        assert lib.epl_workspace_bytes(ctypes.byref(epl.config(R, E, k, 64, Tr))) == want
+        want_bytes = 4 * (E * nblk + nblk * R + E + nblk + E * R + T)
+        assert lib.epl_workspace_bytes(ctypes.byref(epl.config(R, E, k, 64, Tr))) == want_bytes
 
 
 def test_dispatch_errors(lib):
