@@ -153,3 +153,13 @@ def test_debug_errors(lib):
     assert lib.epl_debug_f32_to_e4m3(Fake.ptr(1), Fake.ptr(2), -1, None) == INVALID
     assert lib.epl_debug_f32_to_bf16(None, Fake.ptr(2), 5, None) == INVALID
     assert lib.epl_debug_f32_to_bf16(Fake.ptr(1, 2), Fake.ptr(2), 5, None) == ALIGN
+
+
+def test_binding_rejects_host_tensors_before_any_call():
+    """The Python binding only marshals: a CPU tensor is refused before the library is entered."""
+    import torch
+    cfg_ = epl.config(2, 4, 2, 64, 3)
+    with pytest.raises(ValueError):
+        epl.layout(cfg_, torch.zeros(6, 2, dtype=torch.int32))
+    with pytest.raises(ValueError):
+        epl.debug_f32_to_e4m3(torch.zeros(4))

@@ -1,0 +1,166 @@
+"""GPU behaviour beyond element parity:
+* graph capture and replay;
+* bitwise determinism of dispatch and combine;
+* no stores past the P packed rows at full size;
+* non-default streams;
+* the paper's other model shapes: Qwen3-30B (hidden 2048, 128 experts) and GLM-4.7 (hidden 5120,
+  160 routed experts), from the model-configuration table.
+
+Every comparison is against the CPU oracle or against an eager run of the same HIP path.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_06202_amd import epl
+from paper_2607_06202_amd import workloads as W
+from tests.gpu_util import assert_layout_equal, bf16_bits, bf16_ulp_distance, device, run_layout, to_dev_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(R, E, k, Tr, H, seed, dev):
+    T = R * Tr
+    idx = W.distinct_uniform(seed, np.arange(T), k, E).astype(np.int32)
+    x = W.normal_bf16(seed, W.STREAM_X, T * H).reshape(T, H)
+    gw = W.softmax_gate_weights(seed, T, k)
+    return idx, x, gw, torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev), torch.from_numpy(gw).to(dev)
+
+
+def test_graph_capture_replays_match_eager():
+    """The three calls allocate nothing and issue no memsets, so they can be captured in a graph.
+    Replays with eager work in between must match the eager result every time."""
+    dev = device()
+    R, E, k, Tr, H = 16, 64, 8, 24, 1024
+    idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 3, dev)
+    cfg = epl.config(R, E, k, H, Tr)
+    L = epl.alloc_layout(cfg, dev)
+    recv, _ = epl.alloc_recv(cfg, dev)
+    out = torch.empty(R * Tr, H, dtype=torch.bfloat16, device=dev)
+
+    def layer():
+        epl.layout(cfg, idx_d, out=L)
+        epl.dispatch(cfg, x_d, L, recv)
+        epl.combine(cfg, recv, w_d, L, out)
+
+    layer()
+    torch.cuda.synchronize()
+    want_rows = L.pair_row.clone()
+    want_out = out.clone()
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s):
+        layer()  # warm the capture stream
+    torch.cuda.current_stream(dev).wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        layer()
+    for rep in range(4):
+        L.pair_row.fill_(-5)
+        out.zero_()
+        recv.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(L.pair_row, want_rows), "replay %d: layout differs" % rep
+        assert torch.equal(out.view(torch.int16), want_out.view(torch.int16)), "replay %d: combine differs" % rep
+        _ = (x_d.float() * 2).sum()  # unrelated eager work between replays
+    ref = oracle.layout(R, E, k, Tr, idx)
+    np.testing.assert_array_equal(want_rows.cpu().numpy(), ref.pair_row)
+
+
+def test_dispatch_and_combine_bitwise_deterministic():
+    dev = device()
+    w = W.WORKLOADS["skewed_fp8_ep64"]
+    R, E, k, Tr, H = w.R, w.E, w.k, 32, w.H
+    idx = W.zipf_group_limited(0, R * Tr, E, R, k).astype(np.int32)
+    x = W.normal_bf16(2, W.STREAM_X, R * Tr * H).reshape(R * Tr, H)
+    gw = W.softmax_gate_weights(2, R * Tr, k)
+    idx_d, x_d, w_d = torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev), torch.from_numpy(gw).to(dev)
+    for payload in ["bf16", "fp8"]:
+        cfg = epl.config(R, E, k, H, Tr, payload)
+        L = epl.layout(cfg, idx_d)
+        outs = []
+        for _ in range(3):
+            recv, sc = epl.dispatch(cfg, x_d, L)
+            y = recv if payload == "bf16" else torch.ones(recv.shape, dtype=torch.bfloat16, device=dev)
+            o = epl.combine(cfg, y, w_d, L)
+            torch.cuda.synchronize()
+            P = int(L.expert_off[-1])
+            outs.append((recv[:P].clone(), None if sc is None else sc[:P].clone(), o.clone()))
+        for r, s_, o in outs[1:]:
+            assert torch.equal(r.view(torch.uint8), outs[0][0].view(torch.uint8))
+            assert s_ is None or torch.equal(s_, outs[0][1])
+            assert torch.equal(o.view(torch.int16), outs[0][2].view(torch.int16))
+
+
+def test_full_size_decode_writes_nothing_past_P():
+    dev = device()
+    w = W.WORKLOADS["decode_ep64"]
+    idx = W.routing(w)
+    idx[::97, 3] = -1  # some invalid pairs so that P < T*k
+    idx_d = torch.from_numpy(idx).to(dev)
+    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr)
+    L = epl.layout(cfg, idx_d)
+    cap = w.T * w.k
+    recv = torch.full((cap, w.H), -9.0, dtype=torch.bfloat16, device=dev)
+    x_d = W.device_normal_bf16((w.T, w.H), seed=5, device=dev)
+    epl.dispatch(cfg, x_d, L, recv)
+    torch.cuda.synchronize()
+    P = int(L.expert_off[-1])
+    assert P == cap - len(idx[::97])
+    assert bool((recv[P:].float() == -9.0).all()), "dispatch wrote past the packed rows"
+    ref = oracle.layout(w.R, w.E, w.k, w.Tr, idx)
+    assert_layout_equal(L, ref, "decode with invalid ids")
+
+
+def test_side_stream_dispatch_and_combine():
+    dev = device()
+    R, E, k, Tr, H = 8, 32, 4, 40, 512
+    idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 9, dev)
+    cfg = epl.config(R, E, k, H, Tr)
+    side = torch.cuda.Stream(device=dev)
+    with torch.cuda.stream(side):
+        L = epl.layout(cfg, idx_d)
+        recv, _ = epl.dispatch(cfg, x_d, L)
+        out = epl.combine(cfg, recv, w_d, L)
+    side.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    rr = oracle.dispatch_bf16(x, ref.pair_row, ref.P)
+    np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), rr)
+    np.testing.assert_array_equal(bf16_bits(out), oracle.combine(rr, gw, ref.pair_row))
+
+
+@pytest.mark.parametrize("name,R,E,H,Tr", [("qwen3_30b_ep16", 16, 128, 2048, 64), ("glm47_ep32", 32, 160, 5120, 16),
+                                           ("glm47_ep160", 160, 160, 5120, 4)])
+@pytest.mark.parametrize("payload", ["bf16", "fp8"])
+def test_other_model_shapes(name, R, E, H, Tr, payload):
+    """Shapes of the paper's other evaluated models, top-8, with uniform routing. GLM-4.7's 160
+    experts are placed on 32 ranks (5 each) or 160 ranks (1 each)."""
+    dev = device()
+    k = 8
+    idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 11, dev)
+    cfg = epl.config(R, E, k, H, Tr, payload)
+    L = epl.layout(cfg, idx_d)
+    recv, sc = epl.dispatch(cfg, x_d, L)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    assert_layout_equal(L, ref, name)
+    if payload == "bf16":
+        np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), oracle.dispatch_bf16(x, ref.pair_row, ref.P))
+        y = recv
+        yh = bf16_bits(recv[:ref.P])
+    else:
+        q, s = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(recv[:ref.P].cpu().numpy(), q)
+        np.testing.assert_array_equal(sc[:ref.P].cpu().numpy().view(np.uint32), s.view(np.uint32))
+        yh = W.normal_bf16(12, W.STREAM_Y, ref.P * H).reshape(ref.P, H)
+        y = to_dev_bf16(yh, dev)
+    out = epl.combine(cfg, y, w_d, L)
+    torch.cuda.synchronize()
+    want = oracle.combine(yh, gw, ref.pair_row)
+    got = bf16_bits(out)
+    assert bf16_ulp_distance(got, want).max() <= 1
+    assert (got == want).all()
