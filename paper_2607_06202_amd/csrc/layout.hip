@@ -51,13 +51,23 @@ __global__ void __launch_bounds__(kLayoutThreads)
   const int np = nt * G.k;
   const int64_t g0 = (int64_t)s * G.Tr + t0;
 
+  // Issue the global loads first; their latency overlaps the LDS clearing and the barrier.
+  const int32_t* src = idx + g0 * G.k;
+  int ids[kChunkSlots];
+#pragma unroll
+  for (int q = 0; q < kChunkSlots; ++q) {
+    const int i = tid + q * kLayoutThreads;
+    ids[q] = i < np ? src[i] : 0;
+  }
   for (int i = tid; i < G.E + G.R; i += kLayoutThreads) lds[i] = 0;
   __syncthreads();
 
-  const int32_t* src = idx + g0 * G.k;
   int my_inval = 0;
-  for (int i = tid; i < np; i += kLayoutThreads) {
-    const int e = src[i];
+#pragma unroll
+  for (int q = 0; q < kChunkSlots; ++q) {
+    const int i = tid + q * kLayoutThreads;
+    if (i >= np) break;
+    const int e = ids[q];
     const bool ok = (unsigned)e < (unsigned)G.E;
     dst[i] = ok ? small_div(e, G.inv_El) : -1;
     if (ok)
@@ -189,7 +199,18 @@ __global__ void __launch_bounds__(kLayoutThreads)
   const int np = nt * G.k;
   const int64_t g0 = (int64_t)s * G.Tr + t0;
 
-  // All global inputs of this workgroup are independent: issue them together.
+  // All global inputs of this workgroup are independent: issue them together. That includes
+  // the first entries of this workgroup's slice of segment offsets, which are stored at the end.
+  const int nseg = G.E * G.R;
+  const int seg_per = (nseg + G.nblk - 1) / G.nblk;
+  const int seg_i1 = min(nseg, (b + 1) * seg_per);
+  constexpr int kSegSlots = 2;
+  int seg_pre[kSegSlots];
+#pragma unroll
+  for (int q = 0; q < kSegSlots; ++q) {
+    const int i = b * seg_per + tid + q * kLayoutThreads;
+    seg_pre[q] = i < seg_i1 ? seg_rel[i] : 0;
+  }
   const int32_t* src = idx + g0 * G.k;
   for (int i = tid; i < np; i += kLayoutThreads) {
     const int e = src[i];
@@ -321,10 +342,13 @@ __global__ void __launch_bounds__(kLayoutThreads)
     for (int e = tid; e <= G.E; e += kLayoutThreads) expert_off[e] = eoff[e];
     for (int d = tid; d <= G.R; d += kLayoutThreads) rank_off[d] = eoff[d * G.El];
   }
-  const int n = G.E * G.R;
-  const int per = (n + G.nblk - 1) / G.nblk;
-  const int i1 = min(n, (b + 1) * per);
-  for (int i = b * per + tid; i < i1; i += kLayoutThreads) seg_off[i] = eoff[small_div(i, G.inv_R)] + seg_rel[i];
+#pragma unroll
+  for (int q = 0; q < kSegSlots; ++q) {
+    const int i = b * seg_per + tid + q * kLayoutThreads;
+    if (i < seg_i1) seg_off[i] = eoff[small_div(i, G.inv_R)] + seg_pre[q];
+  }
+  for (int i = b * seg_per + tid + kSegSlots * kLayoutThreads; i < seg_i1; i += kLayoutThreads)
+    seg_off[i] = eoff[small_div(i, G.inv_R)] + seg_rel[i];
 }
 
 // ------------------------------------------------------------------------------------ host
