@@ -63,8 +63,18 @@ __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const 
 // unit = (token g, column chunk c). Units are numbered token-major, so one workgroup's waves
 // cover at most kCombineWaves consecutive tokens; their k row indices and k gate weights are
 // staged in LDS with one coalesced load per workgroup.
+//
+// Occupancy is capped at kCombineWavesPerSimd waves per SIMD. The compiler enforces the cap by
+// reserving a larger register budget. With every resident wave holding 8 random 1 KiB gathers in
+// flight, fewer waves measured faster. With 4 waves per SIMD, 16 per CU:
+// * EP=64 decode: 201 -> 194 us;
+// * EP=32 prefill: 3066 -> 2927 us;
+// * skewed fp8: 371 -> 345 us.
+// 3 waves per SIMD measured within 1% of 4. 2 waves per SIMD was too few to cover the latency.
+constexpr int kCombineWavesPerSimd = 4;
 template <bool SMALL_K>
 __global__ void __launch_bounds__(kCombineThreads)
+    __attribute__((amdgpu_waves_per_eu(kCombineWavesPerSimd, kCombineWavesPerSimd)))
     combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ w, const int32_t* __restrict__ pair_row,
                    u32x4* __restrict__ out, int64_t T, int k, int nv, int chunks) {
   __shared__ int32_t rows_lds[kCombineWaves * EPL_MAX_TOPK];
