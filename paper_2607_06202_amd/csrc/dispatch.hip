@@ -29,7 +29,9 @@ constexpr int kBf16Cols = kWave * kBf16VPL;     // 256 vectors = 4 KiB of a row
 // guard the row. Measured on MI355X, layout -> dispatch -> combine back to back:
 // * bf16 rows: sc1 beat default-policy stores. Nontemporal stores were slower, because they
 //   make the dispatch pay its whole write cost before the next kernel can start.
-// * fp8 rows: sc1+nt beat both.
+// * fp8 rows: sc1+nt beat both. The fp8 scales are partial-line writes of 32 bytes per row and
+//   pass. For them, plain stores measured faster than nontemporal ones (dispatch 235 -> 230 us,
+//   skewed fp8 EP=64).
 template <int POLICY>
 __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int nv, int v) {
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(row_base, 0, nv * 16, kBufferRsrcWord3);
@@ -116,11 +118,21 @@ __device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, c
     const int row = __builtin_amdgcn_readlane(my_row, j);
     if (row < 0 || row >= cap) continue;
     if (on) store_row_policy<kCachePolicySc1Nt>(q, recv + (int64_t)row * nvq, nvq, vq);
-    if (scale_lane) __builtin_nontemporal_store(s, recv_scale + (int64_t)row * NB + vq / 8);
+    if (scale_lane) recv_scale[(int64_t)row * NB + vq / 8] = s;
   }
 }
 
-__global__ void __launch_bounds__(kDispatchThreads)
+// The fp8 kernel is capped at kFp8WavesPerSimd waves per SIMD. The compiler enforces the cap by
+// reserving a larger register budget. Each wave writes up to k scattered 1 KiB q rows per 2 KiB of
+// input, so fewer resident waves keep fewer concurrent random writes in flight. Skewed fp8 EP=64,
+// dispatch alone, input read from HBM:
+// * 8 waves (uncapped): 246.3 us;
+// * 4 waves: 244.5 us;
+// * 3 waves: 240.1 us;
+// * 2 waves: 234.2 us.
+// 1 wave per SIMD was about 30% slower than 2. The bf16 kernel measured best uncapped.
+constexpr int kFp8WavesPerSimd = 2;
+__global__ void __launch_bounds__(kDispatchThreads) __attribute__((amdgpu_waves_per_eu(kFp8WavesPerSimd, kFp8WavesPerSimd)))
     dispatch_fp8_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
                         float* __restrict__ recv_scale, int64_t T, int k, int H, int npass, int64_t cap) {
   const int lane = threadIdx.x % kWave;
