@@ -4,7 +4,8 @@
 A step is one pass of the whole hot path over one synthetic batch:
   epl_layout (routing layout) -> epl_dispatch (row scatter) -> epl_combine (gather-reduce),
 with identity experts in between (combine reads the receive buffer). All inputs are resident
-in HBM before timing starts.
+in HBM before timing starts. The token matrix x is read from byte-identical copies in turn, at
+least 512 MB in total, so that no step finds its input in the 256 MB memory-side cache.
 
 Default workload: EP=64 decode. 64 virtual ranks, 256 experts (4 per rank), top-8, 128
 tokens per rank (8192 tokens), hidden 7168 bf16, uniform routing without replacement, softmax
@@ -32,6 +33,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "dispatch+combine µs/MoE layer and effective HBM GB/s (% of peak), EP=64 decode"
 HBM_PEAK_GBS = 8000.0
+X_ROTATION_BYTES = 512 << 20  # twice the MI355X memory-side cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 CSRC = os.path.join(ROOT, "paper_2607_06202_amd", "csrc")
 
@@ -151,7 +153,6 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="decode_ep64")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cold-steps", type=int, default=30, help="extra cold-cache steps (0 to skip)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time (0 to skip)")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
     ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
@@ -206,6 +207,12 @@ def main():
 
     idx_d = torch.from_numpy(idx).to(dev)
     x_d = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
+    # Byte-identical copies of x at distinct addresses, used in turn, at least twice the
+    # 256 MB memory-side cache (MALL) in total: every step's dispatch then reads its input from
+    # HBM instead of finding the previous step's x still cached.
+    x_bytes = x_d.numel() * x_d.element_size()
+    n_x = max(2, -(-X_ROTATION_BYTES // x_bytes)) if x_bytes else 1
+    xs = [x_d] + [x_d.clone() for _ in range(n_x - 1)]
     w_d = torch.from_numpy(gw).to(dev)
     L = epl.alloc_layout(cfg, dev)
     recv, recv_scale = epl.alloc_recv(cfg, dev)
@@ -217,13 +224,13 @@ def main():
     else:
         y = recv
 
-    def step(ev=None):
+    def step(i, ev=None):
         if ev is not None:
             ev[0].record(stream)
         epl.layout(cfg, idx_d, out=L)
         if ev is not None:
             ev[1].record(stream)
-        epl.dispatch(cfg, x_d, L, recv, recv_scale)
+        epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
         if ev is not None:
             ev[2].record(stream)
         epl.combine(cfg, y, w_d, L, out)
@@ -239,7 +246,7 @@ def main():
     # Warm-up, instrumented: it also picks the dominant call for the roofline entry.
     wev = timed_events(max(args.warmup, 1))
     for i in range(max(args.warmup, 1)):
-        step(wev[i])
+        step(i, wev[i])
     torch.cuda.synchronize()
     P = int(L.expert_off[-1].item())
     wper = per_call_us(wev).mean(axis=0)
@@ -256,7 +263,7 @@ def main():
         epl.layout(cfg, idx_d, out=L)
         if ev is not None and dom == "dispatch":
             ev[0].record(stream)
-        epl.dispatch(cfg, x_d, L, recv, recv_scale)
+        epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
         if ev is not None:
             ev[1 if dom == "dispatch" else 0].record(stream)
         epl.combine(cfg, y, w_d, L, out)
@@ -270,7 +277,7 @@ def main():
     # Per-call breakdown: a separate instrumented pass (events between every call).
     bev = timed_events(args.steps)
     for i in range(args.steps):
-        step(bev[i])
+        step(i, bev[i])
     torch.cuda.synchronize()
     per = per_call_us(bev)
     us_layout, us_dispatch, us_combine = per.mean(axis=0).tolist()
@@ -286,35 +293,6 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": load_traffic(kname, w.name), "algorithmic_bytes": nbytes[dom],
                 "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev)}
-
-    cold = None
-    if args.cold_steps > 0:
-        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)  # 1 GiB, evicts L2 and MALL
-        cper = []
-        for _ in range(args.cold_steps):
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-            flush.zero_()
-            ev[0].record(stream)
-            epl.layout(cfg, idx_d, out=L)
-            ev[1].record(stream)
-            flush.zero_()
-            ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            ev2[0].record(stream)
-            epl.dispatch(cfg, x_d, L, recv, recv_scale)
-            ev2[1].record(stream)
-            flush.zero_()
-            ev3 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            ev3[0].record(stream)
-            epl.combine(cfg, y, w_d, L, out)
-            ev3[1].record(stream)
-            torch.cuda.synchronize()
-            cper.append([ev[0].elapsed_time(ev[1]), ev2[0].elapsed_time(ev2[1]), ev3[0].elapsed_time(ev3[1])])
-        c = np.median(np.array(cper), axis=0) * 1e3
-        cold = {"us_layout": round(float(c[0]), 2), "us_dispatch": round(float(c[1]), 2),
-                "us_combine": round(float(c[2]), 2), "us_per_layer": round(float(c.sum()), 2),
-                "GBps": round(nbytes["total"] / (c.sum() * 1e-6) / 1e9, 1),
-                "note": "median over steps; 1 GiB write before each call, outside the timed events"}
-        del flush
 
     cpu = None
     if args.cpu_budget > 0:
@@ -334,7 +312,7 @@ def main():
         "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_instrumented": round(us_layer_events, 2),
         "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2), "us_combine": round(us_combine, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
-        "roofline": roofline, "cold": cold, "cpu_baseline": cpu,
+        "roofline": roofline, "x_copies": n_x, "cpu_baseline": cpu,
     }
     print(json.dumps(rec))
 
