@@ -109,7 +109,8 @@ size_t epl_workspace_bytes(const epl_config *cfg);
 
 /* Routing layout: per-(source rank, expert) histogram, CalCumSum prefix scans, stable slot
  * assignment and per-token destination-rank dedup (Background phases 3 and 5; Kernel
- * Decomposition: TokenCnt and CalCumSum).
+ * Decomposition: TokenCnt and CalCumSum). It takes one kernel launch up to moderate sizes
+ * (see epl_layout_launches) and three beyond; both give the same outputs.
  *   topk_idx  [T*k] int32, row-major [T][k], read-only.
  *   L         output buffers above, fully overwritten (recv_src/recv_j: rows 0..P-1 only).
  *   workspace device scratch of at least epl_workspace_bytes(cfg), 4-byte aligned; its contents
@@ -150,6 +151,11 @@ epl_status epl_combine(const epl_config *cfg, const void *y, const float *topk_w
  * in [n] fp32, out [n] bytes / bf16 bit patterns, 4-byte aligned; n >= 0.                   */
 epl_status epl_debug_f32_to_e4m3(const float *in, uint8_t *out, int64_t n, void *stream);
 epl_status epl_debug_f32_to_bf16(const float *in, uint16_t *out, int64_t n, void *stream);
+
+/* Number of kernel launches epl_layout issues for cfg: 1 (each workgroup recomputes the global
+ * counts it needs; used while T*k <= 16384, Tr*k <= 4096 and its LDS fits in 64 KiB) or 3
+ * (histogram, scan, finalize). Returns -1 if cfg is invalid. Host-only, no HIP calls.        */
+int epl_layout_launches(const epl_config *cfg);
 
 /* Static strings; never NULL. */
 const char *epl_status_str(epl_status status);

@@ -148,4 +148,9 @@ EPL_EXPORT const char* epl_status_str(epl_status s) {
   return "EPL: unknown status";
 }
 
+EPL_EXPORT int epl_layout_launches(const epl_config* cfg) {
+  if (check_config(cfg) != EPL_OK) return -1;
+  return epl::layout_single(make_geom(cfg)) ? 1 : 3;
+}
+
 EPL_EXPORT const char* epl_version(void) { return "epl 0.1.0 (gfx950)"; }

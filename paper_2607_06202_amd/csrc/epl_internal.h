@@ -18,6 +18,13 @@ constexpr int kLayoutWaves = kLayoutThreads / kWave;
 // always holds whole tokens.
 constexpr int kMaxChunkPairs = 1024;
 constexpr int kChunkSlots = kMaxChunkPairs / kLayoutThreads;  // register slots per lane
+// The single-launch layout reads all T*k ids in every workgroup and walks each source rank's
+// earlier tokens again, so it is used only up to these sizes; larger layouts take three launches.
+// Measured on MI355X, the one-launch layout costs about 11 us + 12 us per 64K pairs, against
+// 17-22 us for three launches: it wins up to about 37K pairs.
+constexpr int64_t kSingleMaxPairs = 16384;     // T*k
+constexpr int64_t kSingleMaxRankPairs = 4096;  // Tr*k
+constexpr size_t kSingleMaxLds = 64 * 1024;    // bytes of LDS per workgroup
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -151,6 +158,8 @@ __device__ __forceinline__ float bf16lo_to_f32(uint32_t w) { return __uint_as_fl
 __device__ __forceinline__ float bf16hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // ---------------------------------------------------------------- launchers (host side)
+size_t single_lds_bytes(const Geom& g);
+bool layout_single(const Geom& g);  // true if epl_layout runs as one launch for this geometry
 hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
                          int32_t* expert_off, int32_t* rank_off, int32_t* seg_off, int32_t* tok_nranks,
                          int32_t* pair_row, int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j,

@@ -84,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.epl_status_str.argtypes = [ctypes.c_int]
         L.epl_version.restype = ctypes.c_char_p
         L.epl_version.argtypes = []
+        L.epl_layout_launches.restype = ctypes.c_int
+        L.epl_layout_launches.argtypes = [CP]
         _lib = L
     return _lib
 
@@ -214,6 +216,14 @@ def debug_f32_to_bf16(v: torch.Tensor) -> torch.Tensor:
     _check(lib().epl_debug_f32_to_bf16(v.data_ptr(), out.data_ptr(), v.numel(), _stream(v.device)),
            "epl_debug_f32_to_bf16")
     return out
+
+
+def layout_launches(cfg: Config) -> int:
+    """Kernel launches epl_layout issues for cfg: 1 (single-launch layout) or 3."""
+    n = lib().epl_layout_launches(ctypes.byref(cfg))
+    if n < 0:
+        raise EplError(1, "epl_layout_launches")
+    return n
 
 
 def version() -> str:

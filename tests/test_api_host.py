@@ -12,6 +12,7 @@ import re
 import pytest
 
 from paper_2607_06202_amd import epl
+from paper_2607_06202_amd import workloads as W
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "epl.h")
@@ -39,6 +40,23 @@ def test_exports_every_declared_symbol(lib):
             "epl_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), "libepl.so does not export " + n
+
+
+def test_layout_launch_count():
+    """One launch up to T*k = 16384, Tr*k = 4096 and 64 KiB of LDS; three beyond."""
+    for name, want in [("tiny", 1), ("decode_ep64", 3), ("prefill_ep32", 3), ("skewed_fp8_ep64", 3),
+                       ("large_ep256", 3)]:
+        w = W.WORKLOADS[name]
+        assert epl.layout_launches(epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)) == want, name
+    assert epl.layout_launches(epl.config(32, 256, 8, 64, 64)) == 1      # T*k = 16384
+    assert epl.layout_launches(epl.config(32, 256, 8, 64, 65)) == 3      # T*k = 16640
+    assert epl.layout_launches(epl.config(2, 16, 8, 64, 512)) == 1       # Tr*k = 4096
+    assert epl.layout_launches(epl.config(2, 16, 8, 64, 513)) == 3       # Tr*k = 4104
+    assert epl.layout_launches(epl.config(64, 1024, 8, 64, 32)) == 1     # LDS 53.5 KiB
+    assert epl.layout_launches(epl.config(1024, 1024, 2, 64, 2)) == 3    # LDS 76 KiB
+    assert epl.layout_launches(epl.config(2, 16, 8, 64, 0)) == 1         # no tokens
+    with pytest.raises(epl.EplError):
+        epl.layout_launches(epl.config(3, 16, 8, 64, 4))                 # E % R != 0
 
 
 def test_version_and_status_strings(lib):

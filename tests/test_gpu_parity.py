@@ -69,6 +69,36 @@ def test_layout_chunked_ragged_and_max_experts():
         assert_layout_equal(L, oracle.layout(R, E, k, Tr, idx), "case %d" % i)
 
 
+@pytest.mark.parametrize("R,E,k,Tr,launches", [
+    (16, 64, 8, 100, 1),    # many chunks per rank, ragged last chunk
+    (64, 1024, 8, 32, 1),   # E = 1024
+    (4, 64, 32, 100, 1),    # k = 32: fifty 2-token chunks per rank
+    (8, 8, 1, 500, 1),      # k = 1
+    (32, 256, 8, 64, 1),    # T*k = 16384, the single-launch limit
+    (32, 256, 8, 65, 3),    # T*k above the limit
+    (64, 256, 8, 300, 3),   # decode-like, three launches
+    (2, 16, 8, 1000, 3),    # Tr*k above the limit
+    (1024, 1024, 2, 2, 3),  # LDS above the limit
+])
+@pytest.mark.parametrize("vec_ids", [True, False])
+def test_layout_both_launch_paths(R, E, k, Tr, launches, vec_ids):
+    """The one-launch and three-launch layouts against the oracle. The ids sit at a 16-byte
+    aligned address (vector loads in the one-launch pass) or 4 bytes past one (scalar loads)."""
+    dev = device()
+    cfg = epl.config(R, E, k, 64, Tr)
+    assert epl.layout_launches(cfg) == launches
+    T = R * Tr
+    idx = W.with_replacement(700 + R + k, T, k, -1, E + 1).astype(np.int32)  # duplicates and invalid ids
+    buf = torch.zeros(T * k + 1, dtype=torch.int32, device=dev)
+    off = 0 if vec_ids else 1
+    idx_d = buf[off:off + T * k].view(T, k)
+    idx_d.copy_(torch.from_numpy(idx))
+    assert idx_d.data_ptr() % 16 == (0 if vec_ids else 4)
+    L = epl.layout(cfg, idx_d)
+    torch.cuda.synchronize()
+    assert_layout_equal(L, oracle.layout(R, E, k, Tr, idx), "R=%d E=%d k=%d Tr=%d" % (R, E, k, Tr))
+
+
 def test_layout_empty_and_all_invalid():
     dev = device()
     w = W.Workload("empty", 4, 8, 3, 0, 64, "bf16", "-")
