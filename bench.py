@@ -249,7 +249,7 @@ def main():
         step(i, wev[i])
     torch.cuda.synchronize()
     P = int(L.expert_off[-1].item())
-    wper = per_call_us(wev).mean(axis=0)
+    wper = np.median(per_call_us(wev), axis=0)  # robust to a slow first step
     dom = "dispatch" if wper[1] >= wper[2] else "combine"
 
     # Timed region: K plain steps. Every 10th step brackets only the dominant call with two HIP
@@ -283,8 +283,17 @@ def main():
     us_layout, us_dispatch, us_combine = per.mean(axis=0).tolist()
     us_layer_events = float(per.sum(axis=1).mean())
 
+    pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
+    percentiles = {"layout": pct(per[:, 0]), "dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]),
+                   "layer": pct(per.sum(axis=1))}
+
     nbytes = algorithmic_bytes(w.T, w.k, w.H, w.R, w.E, P, w.payload)
     value = nbytes["total"] / (ms_per_step * 1e-3) / 1e9
+    # Bytes a multi-GPU dispatch would put on the fabric: one row per (token, destination rank)
+    # pair after dedup, excluding a token's own rank (rank_cnt off the diagonal).
+    rc = L.rank_cnt.cpu().numpy().astype(np.int64)
+    fabric_pairs = int(rc.sum() - np.trace(rc))
+    row_bytes = w.H * 2 if w.payload == "bf16" else w.H + (w.H // 128) * 4
 
     achieved = nbytes[dom] / (dom_us * 1e-6) / 1e9
     kname = {"dispatch": "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
@@ -312,6 +321,8 @@ def main():
         "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_instrumented": round(us_layer_events, 2),
         "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2), "us_combine": round(us_combine, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
+        "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
+        "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,
         "roofline": roofline, "x_copies": n_x, "cpu_baseline": cpu,
     }
     print(json.dumps(rec))

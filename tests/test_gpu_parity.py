@@ -225,6 +225,39 @@ def test_combine_parity(R, E, k, Tr, H, seed):
     assert (got == want).all(), "combine within 1 ulp but %d elements not bit-exact" % (got != want).sum()
 
 
+# ---------------------------------------------------------------------- extreme hidden sizes
+@pytest.mark.parametrize("H,payload", [(8, "bf16"), (128, "fp8"), (1 << 20, "bf16"), (1 << 20, "fp8")])
+def test_extreme_hidden_sizes(H, payload):
+    """The smallest hidden size of each payload (one 16-byte vector per bf16 row, one 128-element
+    block per fp8 row) and EPL_MAX_HIDDEN. Dispatch and combine compared element by element."""
+    dev = device()
+    R, E, k, Tr, seed = 2, 4, 3, 3, 7
+    T = R * Tr
+    idx = W.with_replacement(seed, T, k, -1, E + 1).astype(np.int32)
+    x = W.normal_bf16(seed, W.STREAM_X, T * H).reshape(T, H)
+    if payload == "fp8":
+        x[:2] = _adversarial_rows(H, 2, seed)
+    gw = W.softmax_gate_weights(seed, T, k)
+    w = W.Workload("h", R, E, k, Tr, H, payload, "-")
+    cfg, L = run_layout(w, idx, dev)
+    ref = oracle.layout(R, E, k, Tr, idx)
+    recv, scale = epl.dispatch(cfg, to_dev_bf16(x, dev), L)
+    torch.cuda.synchronize()
+    if payload == "bf16":
+        rr = oracle.dispatch_bf16(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), rr)
+        y, yh = recv, rr
+    else:
+        q, sc = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(recv[:ref.P].cpu().numpy(), q)
+        np.testing.assert_array_equal(scale[:ref.P].cpu().numpy().view(np.uint32), sc.view(np.uint32))
+        yh = W.normal_bf16(seed, W.STREAM_Y, max(ref.P, 1) * H).reshape(-1, H)
+        y = to_dev_bf16(yh, dev)
+    out = epl.combine(cfg, y, torch.from_numpy(gw).to(dev), L)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bf16_bits(out), oracle.combine(yh, gw, ref.pair_row))
+
+
 # ---------------------------------------------------------------------- full-size named workloads
 def _full_inputs(w, dev):
     idx = W.routing(w)
