@@ -7,7 +7,8 @@
 // Token-Reordering). All ranks are virtual here, so the count "exchange" is just reading the
 // [rank][expert] matrix by column.
 //
-// Three launches, no atomics that decide an order, bit-identical on every run:
+// Three launches, no atomics that decide an order, bit-identical on every run (small layouts
+// take one launch instead, route_single below, with the same outputs):
 //   K1 route_hist      one workgroup per chunk (CT whole tokens of one source rank): LDS
 //                      histograms of expert ids and of first-per-token destination ranks, the
 //                      per-token first-pair bitmask, tok_nranks and the invalid count.
@@ -21,7 +22,8 @@
 //                      popcount of the lanes below, per-wave LDS running counts. A cross-wave
 //                      prefix then yields pair_row, recv_src, recv_j and pair_rslot.
 //
-// Small integer quotients (pair -> token, expert -> rank, both numerators < 2^21) use
+// Small integer quotients (pair -> token within a chunk, expert -> rank, seg_off index -> expert;
+// every numerator < 2^21) use
 // q = (int)((n + 0.5f) * (1.0f / d)). The exact quotient sits at least 0.5/d away from an
 // integer, and two float roundings perturb (n + 0.5)/d by at most (n + 0.5) * 2^-22 / d, which is
 // smaller than 0.5/d. So the truncated result is exact.
