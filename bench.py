@@ -50,12 +50,27 @@ def algorithmic_bytes(T, k, H, R, E, P, payload):
             "total": layout + dispatch + combine}
 
 
-def source_hash():
+# The source file that defines each kernel; every kernel also builds against epl_internal.h.
+KERNEL_SOURCES = {"route_hist_kernel": "layout.hip", "route_scan_kernel": "layout.hip",
+                  "route_finalize_kernel": "layout.hip", "route_single_kernel": "layout.hip",
+                  "dispatch_bf16_kernel": "dispatch.hip", "dispatch_fp8_kernel": "dispatch.hip",
+                  "combine_kernel": "combine.hip"}
+
+
+def source_hash(kernel):
+    """Hash of the code a kernel is built from: its source file and the shared header, with
+    comments and whitespace removed, so that a comment edit does not invalidate counter data."""
+    import re
+
     h = hashlib.sha256()
-    for f in sorted(os.listdir(CSRC)):
-        if f.endswith((".hip", ".h")):
-            h.update(f.encode())
-            h.update(open(os.path.join(CSRC, f), "rb").read())
+    files = (KERNEL_SOURCES[kernel], "epl_internal.h") if kernel in KERNEL_SOURCES else sorted(
+        f for f in os.listdir(CSRC) if f.endswith((".hip", ".h")))
+    for f in files:
+        text = open(os.path.join(CSRC, f)).read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(f.encode())
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -67,7 +82,7 @@ def load_traffic(kernel, workload):
     except (OSError, ValueError):
         return None
     ent = rec.get("kernels", {}).get("%s@%s" % (kernel, workload))
-    if not ent or ent.get("source_hash") != source_hash():
+    if not ent or ent.get("source_hash") != source_hash(kernel):
         return None
     return ent.get("bytes_per_launch")
 
@@ -106,17 +121,17 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
              "commands:", *["  " + c for c in command],
              "calibration: 1 GiB device copy reads FETCH_SIZE %.1f KiB (factor %.4f), WRITE_SIZE %.1f KiB (factor %.4f)"
              % (np.median(cf), fetch_factor, np.median(cw), write_factor),
-             "%-40s %8s %14s %14s %16s" % ("kernel", "launches", "FETCH KiB", "WRITE KiB", "HBM bytes (cal.)")]
+             "%-40s %8s %14s %14s %16s  %s" % ("kernel", "launches", "FETCH KiB", "WRITE KiB", "HBM bytes (cal.)",
+                                                "source hash")]
     for name in fetch:
         if not name.startswith("epl::"):
             continue
         short = name.split("::")[1].split("<")[0]
         fk, wk = float(np.mean(fetch[name])), float(np.mean(write.get(name, [0.0])))
         b = fk * 1024 * fetch_factor + wk * 1024 * write_factor
-        rec["kernels"]["%s@%s" % (short, workload)] = {"source_hash": source_hash(), "fetch_kib": fk,
+        rec["kernels"]["%s@%s" % (short, workload)] = {"source_hash": source_hash(short), "fetch_kib": fk,
                                                         "write_kib": wk, "bytes_per_launch": int(round(b))}
-        lines.append("%-40s %8d %14.1f %14.1f %16d" % (name, len(fetch[name]), fk, wk, b))
-    lines.append("source hash of paper_2607_06202_amd/csrc: %s" % source_hash())
+        lines.append("%-40s %8d %14.1f %14.1f %16d  %s" % (name, len(fetch[name]), fk, wk, b, source_hash(short)))
     json.dump(rec, open(TRAFFIC_FILE, "w"), indent=1, sort_keys=True)
     txt = os.path.join(ROOT, "profiles", "hbm_counters_%s.txt" % workload)
     open(txt, "w").write("\n".join(lines) + "\n")
