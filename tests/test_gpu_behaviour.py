@@ -3,8 +3,9 @@
 * bitwise determinism of dispatch and combine;
 * no stores past the P packed rows at full size;
 * non-default streams;
-* the paper's other model shapes: Qwen3-30B (hidden 2048, 128 experts) and GLM-4.7 (hidden 5120,
-  160 routed experts), from the model-configuration table.
+* the paper's other model shapes: Qwen3-30B (hidden 2048, 128 experts), GLM-4.7 (hidden 5120,
+  160 routed experts) and DeepSeek at 128 ranks, from the model-configuration table and the
+  end-to-end deployments.
 
 Every comparison is against the CPU oracle or against an eager run of the same HIP path.
 """
@@ -134,11 +135,12 @@ def test_side_stream_dispatch_and_combine():
 
 
 @pytest.mark.parametrize("name,R,E,H,Tr", [("qwen3_30b_ep16", 16, 128, 2048, 64), ("glm47_ep32", 32, 160, 5120, 16),
-                                           ("glm47_ep160", 160, 160, 5120, 4)])
+                                           ("glm47_ep160", 160, 160, 5120, 4), ("deepseek_ep128", 128, 256, 7168, 16)])
 @pytest.mark.parametrize("payload", ["bf16", "fp8"])
 def test_other_model_shapes(name, R, E, H, Tr, payload):
-    """Shapes of the paper's other evaluated models, top-8, with uniform routing. GLM-4.7's 160
-    experts are placed on 32 ranks (5 each) or 160 ranks (1 each)."""
+    """Shapes of the paper's evaluated deployments, top-8, with uniform routing: Qwen3-30B on 16
+    ranks, GLM-4.7's 160 experts on 32 ranks (5 each) or 160 ranks (1 each), and DeepSeek's 256
+    experts on 128 ranks (2 each)."""
     dev = device()
     k = 8
     idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 11, dev)
