@@ -169,6 +169,8 @@ def main():
     ap.add_argument("--workload", default="decode_ep64")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time (0 to skip)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time HIP graph replays of the layer (one graph per x copy) instead of eager launches")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
     ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from rocprofv3 --pmc runs (no GPU needed)")
@@ -267,13 +269,37 @@ def main():
     wper = np.median(per_call_us(wev), axis=0)  # robust to a slow first step
     dom = "dispatch" if wper[1] >= wper[2] else "combine"
 
+    graphs = None
+    if args.graph:
+        # One captured layer per x copy; capture runs on a side stream after an eager warm-up there.
+        side = torch.cuda.Stream(device=dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            for i in range(n_x):
+                step(i)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graphs = []
+        for i in range(n_x):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(i)
+            graphs.append(g)
+        for i in range(max(args.warmup, 1)):
+            graphs[i % n_x].replay()
+        torch.cuda.synchronize()
+
     # Timed region: K plain steps. Every 10th step brackets only the dominant call with two HIP
-    # events on the library's stream, so the markers barely perturb the wall time.
-    sample = [i for i in range(args.steps) if i % 10 == 0]
+    # events on the library's stream, so the markers barely perturb the wall time. Graph replays
+    # take no markers; the dominant call's duration then comes from the instrumented pass below.
+    sample = [i for i in range(args.steps) if i % 10 == 0] if graphs is None else []
     dev_ev = {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for i in sample}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        if graphs is not None:
+            graphs[i % n_x].replay()
+            continue
         ev = dev_ev.get(i)
         epl.layout(cfg, idx_d, out=L)
         if ev is not None and dom == "dispatch":
@@ -287,7 +313,6 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    dom_us = float(np.mean([a.elapsed_time(b) for a, b in dev_ev.values()]) * 1e3)
 
     # Per-call breakdown: a separate instrumented pass (events between every call).
     bev = timed_events(args.steps)
@@ -297,6 +322,10 @@ def main():
     per = per_call_us(bev)
     us_layout, us_dispatch, us_combine = per.mean(axis=0).tolist()
     us_layer_events = float(per.sum(axis=1).mean())
+    if dev_ev:
+        dom_us = float(np.mean([a.elapsed_time(b) for a, b in dev_ev.values()]) * 1e3)
+    else:
+        dom_us = float(np.mean(per[:, 1 if dom == "dispatch" else 2]))
 
     pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
     percentiles = {"layout": pct(per[:, 0]), "dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]),
@@ -316,7 +345,7 @@ def main():
     roofline = {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": load_traffic(kname, w.name), "algorithmic_bytes": nbytes[dom],
-                "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev)}
+                "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev) if dev_ev else args.steps}
 
     cpu = None
     if args.cpu_budget > 0:
@@ -336,6 +365,7 @@ def main():
         "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_instrumented": round(us_layer_events, 2),
         "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2), "us_combine": round(us_combine, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
+        "launch": "graph" if graphs is not None else "eager",
         "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
         "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,
         "roofline": roofline, "x_copies": n_x, "cpu_baseline": cpu,
