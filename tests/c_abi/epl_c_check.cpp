@@ -1,0 +1,198 @@
+// Standalone C++ consumer of the C ABI in include/epl.h: no Python, no torch. It allocates
+// device buffers with the HIP runtime, runs layout -> dispatch -> combine on its own stream,
+// and compares every output with the CPU oracle (oracle/liboracle.so, test infrastructure),
+// then checks that host-detectable errors are reported before anything is launched.
+// Prints "c abi check ok" and exits 0 on success; prints the first difference and exits 1.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "epl.h"
+
+extern "C" {  // the oracle's entry points (plain C, no header shared with the library)
+int eplref_layout(int R, int E, int k, int Tr, const int32_t* idx, int32_t* send_cnt, int32_t* rank_cnt,
+                  int32_t* expert_off, int32_t* rank_off, int32_t* seg_off, int32_t* tok_nranks, int32_t* pair_row,
+                  int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j, int32_t* num_invalid);
+void eplref_dispatch_bf16(int64_t T, int k, int H, const uint16_t* x, const int32_t* pair_row, uint16_t* recv);
+void eplref_dispatch_fp8(int64_t T, int k, int H, const uint16_t* x, const int32_t* pair_row, uint8_t* recv,
+                         float* recv_scale);
+void eplref_combine(int64_t T, int k, int H, const uint16_t* y, const float* w, const int32_t* pair_row,
+                    const int64_t* tokens, int64_t n_tokens, uint16_t* out);
+}
+
+#define HIP_OK(x)                                                                              \
+  do {                                                                                         \
+    hipError_t e_ = (x);                                                                       \
+    if (e_ != hipSuccess) {                                                                    \
+      std::printf("HIP error %s at line %d\n", hipGetErrorString(e_), __LINE__);               \
+      std::exit(1);                                                                            \
+    }                                                                                          \
+  } while (0)
+
+namespace {
+
+uint64_t splitmix(uint64_t& s) {
+  uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+template <typename T>
+T* dev_copy(const std::vector<T>& h) {
+  T* d = nullptr;
+  HIP_OK(hipMalloc(&d, std::max<size_t>(1, h.size()) * sizeof(T)));
+  if (!h.empty()) HIP_OK(hipMemcpy(d, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice));
+  return d;
+}
+
+template <typename T>
+std::vector<T> host_copy(const T* d, size_t n) {
+  std::vector<T> h(n);
+  if (n) HIP_OK(hipMemcpy(h.data(), d, n * sizeof(T), hipMemcpyDeviceToHost));
+  return h;
+}
+
+template <typename T>
+bool same(const char* what, const std::vector<T>& got, const std::vector<T>& want, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (std::memcmp(&got[i], &want[i], sizeof(T)) != 0) {
+      std::printf("%s differs at %zu\n", what, i);
+      return false;
+    }
+  return true;
+}
+
+struct Case {
+  int R, E, k, Tr, H;
+  epl_payload payload;
+};
+
+bool run_case(const Case& c, uint64_t seed, hipStream_t stream) {
+  const int64_t T = (int64_t)c.R * c.Tr, Tk = T * c.k;
+  const bool fp8 = c.payload == EPL_PAYLOAD_FP8_E4M3;
+  std::vector<int32_t> idx(Tk);
+  for (auto& v : idx) v = (int32_t)(splitmix(seed) % (uint64_t)(c.E + 2)) - 1;  // duplicates and invalid ids
+  std::vector<uint16_t> x((size_t)T * c.H), y((size_t)Tk * c.H);
+  for (auto& v : x) v = (uint16_t)(0x3C00 + (splitmix(seed) % 0x0800) - 0x0400) ^ (uint16_t)((splitmix(seed) & 1) << 15);
+  for (auto& v : y) v = (uint16_t)(0x3F00 + (splitmix(seed) % 0x0200) - 0x0100);
+  std::vector<float> w(Tk);
+  for (auto& v : w) v = (float)(splitmix(seed) % 1000) / 1000.0f - 0.25f;
+
+  epl_config cfg{c.R, c.E, c.k, c.H, c.Tr, c.payload};
+  // reference
+  std::vector<int32_t> r_send(c.R * c.E), r_rank(c.R * c.R), r_eoff(c.E + 1), r_roff(c.R + 1), r_seg(c.E * c.R),
+      r_ntok(T), r_row(Tk), r_slot(Tk), r_src(Tk), r_j(Tk), r_inv(1);
+  if (eplref_layout(c.R, c.E, c.k, c.Tr, idx.data(), r_send.data(), r_rank.data(), r_eoff.data(), r_roff.data(),
+                    r_seg.data(), r_ntok.data(), r_row.data(), r_slot.data(), r_src.data(), r_j.data(), r_inv.data()) != 0) {
+    std::printf("oracle rejected the case\n");
+    return false;
+  }
+  const int32_t P = r_eoff[c.E];
+
+  // device
+  int32_t* d_idx = dev_copy(idx);
+  std::vector<int32_t*> d_out;
+  const size_t sizes[] = {(size_t)c.R * c.E, (size_t)c.R * c.R, (size_t)c.E + 1, (size_t)c.R + 1, (size_t)c.E * c.R,
+                          (size_t)T,         (size_t)Tk,        (size_t)Tk,      (size_t)Tk,      (size_t)Tk,
+                          1};
+  for (size_t n : sizes) {
+    int32_t* p = nullptr;
+    HIP_OK(hipMalloc(&p, std::max<size_t>(n, 1) * 4));
+    d_out.push_back(p);
+  }
+  epl_layout_buffers L{d_out[0], d_out[1], d_out[2], d_out[3], d_out[4], d_out[5],
+                       d_out[6], d_out[7], d_out[8], d_out[9], d_out[10]};
+  const size_t ws_bytes = epl_workspace_bytes(&cfg);
+  void* ws = nullptr;
+  HIP_OK(hipMalloc(&ws, ws_bytes));
+  uint16_t* d_x = dev_copy(x);
+  uint16_t* d_y = dev_copy(y);
+  float* d_w = dev_copy(w);
+  void* d_recv = nullptr;
+  float* d_scale = nullptr;
+  HIP_OK(hipMalloc(&d_recv, (size_t)std::max<int64_t>(Tk, 1) * c.H * (fp8 ? 1 : 2)));
+  if (fp8) HIP_OK(hipMalloc(&d_scale, (size_t)std::max<int64_t>(Tk, 1) * (c.H / 128) * sizeof(float)));
+  uint16_t* d_o = nullptr;
+  HIP_OK(hipMalloc(&d_o, (size_t)std::max<int64_t>(T, 1) * c.H * 2));
+
+  bool ok = epl_layout(&cfg, d_idx, &L, ws, ws_bytes, stream) == EPL_OK &&
+            epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk, stream) == EPL_OK &&
+            epl_combine(&cfg, d_y, d_w, &L, d_o, stream) == EPL_OK;
+  if (!ok) std::printf("a call returned an error status\n");
+  HIP_OK(hipStreamSynchronize(stream));
+
+  const std::vector<int32_t>* refs[] = {&r_send, &r_rank, &r_eoff, &r_roff, &r_seg, &r_ntok, &r_row, &r_slot};
+  const char* names[] = {"send_cnt", "rank_cnt", "expert_off", "rank_off", "seg_off", "tok_nranks", "pair_row",
+                         "pair_rslot"};
+  for (int i = 0; ok && i < 8; ++i) ok = same(names[i], host_copy(d_out[i], sizes[i]), *refs[i], sizes[i]);
+  ok = ok && same("recv_src", host_copy(d_out[8], P), r_src, P) && same("recv_j", host_copy(d_out[9], P), r_j, P) &&
+       same("num_invalid", host_copy(d_out[10], 1), r_inv, 1);
+  if (ok && fp8) {
+    std::vector<uint8_t> q((size_t)Tk * c.H);
+    std::vector<float> s((size_t)Tk * (c.H / 128));
+    eplref_dispatch_fp8(T, c.k, c.H, x.data(), r_row.data(), q.data(), s.data());
+    ok = same("fp8 rows", host_copy((const uint8_t*)d_recv, (size_t)P * c.H), q, (size_t)P * c.H) &&
+         same("fp8 scales", host_copy(d_scale, (size_t)P * (c.H / 128)), s, (size_t)P * (c.H / 128));
+  } else if (ok) {
+    std::vector<uint16_t> rr((size_t)Tk * c.H);
+    eplref_dispatch_bf16(T, c.k, c.H, x.data(), r_row.data(), rr.data());
+    ok = same("bf16 rows", host_copy((const uint16_t*)d_recv, (size_t)P * c.H), rr, (size_t)P * c.H);
+  }
+  if (ok) {
+    std::vector<uint16_t> o((size_t)T * c.H);
+    eplref_combine(T, c.k, c.H, y.data(), w.data(), r_row.data(), nullptr, T, o.data());
+    ok = same("combine", host_copy(d_o, (size_t)T * c.H), o, (size_t)T * c.H);
+  }
+
+  // Host-detectable errors come back before any launch.
+  if (ok) {
+    epl_config bad = cfg;
+    bad.num_experts = c.E + 1;
+    ok = epl_layout(&bad, d_idx, &L, ws, ws_bytes, stream) == EPL_ERR_INVALID_ARG &&
+         epl_layout(&cfg, d_idx, &L, ws, ws_bytes - 4, stream) == EPL_ERR_WORKSPACE &&
+         epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk - 1, stream) == EPL_ERR_CAPACITY &&
+         epl_dispatch(&cfg, d_x, &L, (char*)d_recv + 2, d_scale, Tk, stream) == EPL_ERR_ALIGN &&
+         epl_combine(&cfg, d_y, d_w, &L, (char*)d_o + 8, stream) == EPL_ERR_ALIGN;
+    if (!ok) std::printf("an invalid call was not rejected with the documented status\n");
+  }
+
+  for (int32_t* p : d_out) HIP_OK(hipFree(p));
+  HIP_OK(hipFree(d_idx));
+  HIP_OK(hipFree(ws));
+  HIP_OK(hipFree(d_x));
+  HIP_OK(hipFree(d_y));
+  HIP_OK(hipFree(d_w));
+  HIP_OK(hipFree(d_recv));
+  if (d_scale) HIP_OK(hipFree(d_scale));
+  HIP_OK(hipFree(d_o));
+  std::printf("case R=%d E=%d k=%d Tr=%d H=%d %s layout launches=%d: %s\n", c.R, c.E, c.k, c.Tr, c.H,
+              fp8 ? "fp8" : "bf16", epl_layout_launches(&cfg), ok ? "ok" : "FAILED");
+  return ok;
+}
+
+}  // namespace
+
+int main() {
+  std::printf("%s\n", epl_version());
+  hipStream_t stream;
+  HIP_OK(hipStreamCreate(&stream));
+  const Case cases[] = {
+      {8, 32, 4, 50, 1024, EPL_PAYLOAD_BF16},     // one-launch layout
+      {4, 16, 8, 100, 512, EPL_PAYLOAD_FP8_E4M3},  // fp8, one-launch layout
+      {32, 256, 8, 80, 256, EPL_PAYLOAD_BF16},    // T*k = 20480: three-launch layout
+      {2, 8, 3, 0, 64, EPL_PAYLOAD_BF16},         // no tokens
+  };
+  bool ok = true;
+  uint64_t seed = 12345;
+  for (const Case& c : cases) ok = run_case(c, seed++, stream) && ok;
+  HIP_OK(hipStreamDestroy(stream));
+  if (!ok) return 1;
+  std::printf("c abi check ok\n");
+  return 0;
+}
