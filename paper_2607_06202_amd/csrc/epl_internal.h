@@ -18,6 +18,7 @@ constexpr int kLayoutWaves = kLayoutThreads / kWave;
 // always holds whole tokens.
 constexpr int kMaxChunkPairs = 1024;
 constexpr int kChunkSlots = kMaxChunkPairs / kLayoutThreads;  // register slots per lane
+constexpr int kLayoutSlots = EPL_MAX_EXPERTS / kLayoutThreads;  // per-lane slots covering E or R experts/ranks
 // The single-launch layout reads all T*k ids in every workgroup and walks each source rank's
 // earlier tokens again, so it is used only up to these sizes; larger layouts take three launches.
 // Measured on MI355X, the one-launch layout costs about 11 us + 12 us per 64K pairs, against

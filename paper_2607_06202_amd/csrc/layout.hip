@@ -117,6 +117,8 @@ __global__ void __launch_bounds__(kLayoutThreads)
 }
 
 // ------------------------------------------------------------------------------------ K2
+constexpr int kScanNC = 16;  // chunks per source rank kept in registers (more go through a plain loop)
+
 __global__ void __launch_bounds__(kLayoutThreads)
     route_scan_kernel(Geom G, int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r,
                       const int32_t* __restrict__ inval, int32_t* __restrict__ recv_cnt, int32_t* __restrict__ send_cnt,
@@ -128,12 +130,23 @@ __global__ void __launch_bounds__(kLayoutThreads)
     // Expert column e, laid out [source rank][chunk]: counts -> rows relative to the expert start.
     const int e = b;
     int32_t* col = chunk_e + (int64_t)e * G.nblk;
+    const bool regs = G.NC <= kScanNC;  // uniform: the lane's NC counts fit in registers
     int carry = 0;
     for (int s0 = 0; s0 < G.R; s0 += kLayoutThreads) {
       const int s = s0 + tid;
+      const int sc = min(s, G.R - 1);
+      int h[kScanNC];
       int sum = 0;
-      if (s < G.R)
-        for (int c = 0; c < G.NC; ++c) sum += col[s * G.NC + c];
+      if (regs) {
+        // All NC loads in flight together (index clamped into the lane's run), then one wait.
+#pragma unroll
+        for (int c = 0; c < kScanNC; ++c) h[c] = col[sc * G.NC + min(c, G.NC - 1)];
+#pragma unroll
+        for (int c = 0; c < kScanNC; ++c) sum += c < G.NC ? h[c] : 0;
+      } else {
+        for (int c = 0; c < G.NC; ++c) sum += col[sc * G.NC + c];
+      }
+      if (s >= G.R) sum = 0;
       int total;
       const int excl = block_exclusive_sum(sum, total, scratch);
       if (s < G.R) {
@@ -141,10 +154,19 @@ __global__ void __launch_bounds__(kLayoutThreads)
         seg_rel[e * G.R + s] = base;
         send_cnt[s * G.E + e] = sum;
         int run = base;
-        for (int c = 0; c < G.NC; ++c) {
-          const int h = col[s * G.NC + c];
-          col[s * G.NC + c] = run;
-          run += h;
+        if (regs) {
+#pragma unroll
+          for (int c = 0; c < kScanNC; ++c) {
+            if (c >= G.NC) break;
+            col[s * G.NC + c] = run;
+            run += h[c];
+          }
+        } else {
+          for (int c = 0; c < G.NC; ++c) {
+            const int hc = col[s * G.NC + c];
+            col[s * G.NC + c] = run;
+            run += hc;
+          }
         }
       }
       carry += total;
@@ -153,13 +175,25 @@ __global__ void __launch_bounds__(kLayoutThreads)
   } else if (b < G.E + G.R) {
     // Source rank s: per destination rank r, slots of earlier chunks come first.
     const int s = b - G.E;
+    int32_t* rows = chunk_r + (int64_t)s * G.NC * G.R;  // this rank's NC chunk rows of R counts
     for (int r = tid; r < G.R; r += kLayoutThreads) {
       int run = 0;
-      for (int c = 0; c < G.NC; ++c) {
-        int32_t* p = chunk_r + (int64_t)(s * G.NC + c) * G.R + r;
-        const int h = *p;
-        *p = run;
-        run += h;
+      if (G.NC <= kScanNC) {
+        int h[kScanNC];
+#pragma unroll
+        for (int c = 0; c < kScanNC; ++c) h[c] = rows[(int64_t)min(c, G.NC - 1) * G.R + r];
+#pragma unroll
+        for (int c = 0; c < kScanNC; ++c) {
+          if (c >= G.NC) break;
+          rows[(int64_t)c * G.R + r] = run;
+          run += h[c];
+        }
+      } else {
+        for (int c = 0; c < G.NC; ++c) {
+          const int hc = rows[(int64_t)c * G.R + r];
+          rows[(int64_t)c * G.R + r] = run;
+          run += hc;
+        }
       }
       rank_cnt[s * G.R + r] = run;
     }
@@ -332,30 +366,66 @@ __global__ void __launch_bounds__(kLayoutThreads)
     const int i = b * seg_per + tid + q * kLayoutThreads;
     seg_pre[q] = i < seg_i1 ? seg_rel[i] : 0;
   }
+  // Each lane loads its ids, token masks, chunk counts and expert totals into registers first
+  // (indices clamped, so no load sits behind a branch), then waits once.
   const int32_t* src = idx + g0 * G.k;
-  for (int i = tid; i < np; i += kLayoutThreads) {
-    const int e = src[i];
-    const bool ok = (unsigned)e < (unsigned)G.E;
-    ekey[i] = ok ? e : -1;
-    dkey[i] = ok ? small_div(e, G.inv_El) : -1;
+  const int per = (G.E + kLayoutThreads - 1) / kLayoutThreads;  // experts per lane in the scan below
+  const int e0 = min(G.E, tid * per), e1 = min(G.E, e0 + per);
+  int id_r[kChunkSlots];
+  uint32_t fm_r[kChunkSlots];
+#pragma unroll
+  for (int q = 0; q < kChunkSlots; ++q) {
+    id_r[q] = 0;
+    fm_r[q] = 0;
   }
-  for (int t = tid; t < nt; t += kLayoutThreads) fm[t] = fmask[g0 + t];
-  for (int e = tid; e < G.E; e += kLayoutThreads) base_e[e] = chunk_e[(int64_t)e * G.nblk + b];
-  for (int r = tid; r < G.R; r += kLayoutThreads) base_r[r] = chunk_r[(int64_t)b * G.R + r];
+  if (np > 0) {  // uniform; idx may be null when there are no tokens
+#pragma unroll
+    for (int q = 0; q < kChunkSlots; ++q) {
+      const int i = tid + q * kLayoutThreads;
+      id_r[q] = src[min(i, np - 1)];
+      fm_r[q] = fmask[g0 + min(i, nt - 1)];
+    }
+  }
+  int ce_r[kLayoutSlots], cr_r[kLayoutSlots], rc_r[kLayoutSlots];
+#pragma unroll
+  for (int q = 0; q < kLayoutSlots; ++q) {
+    const int e = tid + q * kLayoutThreads;
+    ce_r[q] = chunk_e[(int64_t)min(e, G.E - 1) * G.nblk + b];
+    cr_r[q] = chunk_r[(int64_t)b * G.R + min(e, G.R - 1)];
+    rc_r[q] = recv_cnt[min(e0 + q, G.E - 1)];
+  }
   for (int i = tid; i < kLayoutWaves * (G.E + G.R); i += kLayoutThreads) whe[i] = 0;
+#pragma unroll
+  for (int q = 0; q < kChunkSlots; ++q) {
+    const int i = tid + q * kLayoutThreads;
+    if (i < np) {
+      const int e = id_r[q];
+      const bool ok = (unsigned)e < (unsigned)G.E;
+      ekey[i] = ok ? e : -1;
+      dkey[i] = ok ? small_div(e, G.inv_El) : -1;
+    }
+    if (i < nt) fm[i] = fm_r[q];
+  }
+#pragma unroll
+  for (int q = 0; q < kLayoutSlots; ++q) {
+    const int e = tid + q * kLayoutThreads;
+    if (e < G.E) base_e[e] = ce_r[q];
+    if (e < G.R) base_r[e] = cr_r[q];
+  }
 
-  // expert_off = exclusive scan of recv_cnt; each thread owns a contiguous run of experts.
+  // expert_off = exclusive scan of recv_cnt; each lane owns the contiguous run [e0, e1).
   {
-    const int per = (G.E + kLayoutThreads - 1) / kLayoutThreads;
-    const int e0 = min(G.E, tid * per), e1 = min(G.E, e0 + per);
     int sum = 0;
-    for (int e = e0; e < e1; ++e) sum += recv_cnt[e];
+#pragma unroll
+    for (int q = 0; q < kLayoutSlots; ++q) sum += e0 + q < e1 ? rc_r[q] : 0;
     int total;
     int run = block_exclusive_sum(sum, total, scratch);  // synchronises the workgroup
-    for (int e = e0; e < e1; ++e) {
-      eoff[e] = run;
-      base_e[e] += run;
-      run += recv_cnt[e];
+#pragma unroll
+    for (int q = 0; q < kLayoutSlots; ++q) {
+      if (e0 + q >= e1) break;
+      eoff[e0 + q] = run;
+      base_e[e0 + q] += run;
+      run += rc_r[q];
     }
     if (tid == 0) eoff[G.E] = total;
   }
