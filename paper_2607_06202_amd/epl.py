@@ -147,6 +147,27 @@ def alloc_layout(cfg: Config, device) -> Layout:
                   torch.empty(ws, dtype=torch.uint8, device=device))
 
 
+def _same_device(dev, **tensors) -> None:
+    for name, t in tensors.items():
+        if t is not None and t.device != dev:
+            raise ValueError("%s is on %s, expected %s" % (name, t.device, dev))
+
+
+def _check_layout(cfg: Config, L: Layout, dev) -> None:
+    """The layout buffers were sized for cfg (the kernels index them by cfg's shape)."""
+    c = L.cfg
+    if (c.num_ranks, c.num_experts, c.topk, c.tokens_per_rank) != (cfg.num_ranks, cfg.num_experts, cfg.topk,
+                                                                    cfg.tokens_per_rank):
+        raise ValueError("layout was allocated for %r, not %r" % (c, cfg))
+    _same_device(dev, pair_row=L.pair_row, workspace=L.workspace)
+
+
+def _rows_of(t: torch.Tensor, name: str, width: int) -> int:
+    if t.dim() != 2 or t.shape[1] != width:
+        raise ValueError("%s must be 2-D with %d columns, got shape %s" % (name, width, tuple(t.shape)))
+    return t.shape[0]
+
+
 def layout(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> Layout:
     """epl_layout: topk_idx [T, k] int32 on the GPU -> Layout."""
     dev = topk_idx.device
@@ -154,9 +175,13 @@ def layout(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> La
     if topk_idx.numel() != cfg.T * cfg.topk:
         raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
     L = out if out is not None else alloc_layout(cfg, dev)
+    _check_layout(cfg, L, dev)
+    if L.workspace.numel() < workspace_bytes(cfg):
+        raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), workspace_bytes(cfg)))
     bufs = L.buffers()
-    _check(lib().epl_layout(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs), L.workspace.data_ptr(),
-                            L.workspace.numel(), _stream(dev)), "epl_layout")
+    with torch.cuda.device(dev):
+        _check(lib().epl_layout(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs), L.workspace.data_ptr(),
+                                L.workspace.numel(), _stream(dev)), "epl_layout")
     return L
 
 
@@ -177,14 +202,24 @@ def dispatch(cfg: Config, x: torch.Tensor, L: Layout, recv: torch.Tensor | None 
     """epl_dispatch: x [T, H] bf16 -> (recv [cap, H] bf16 | uint8, recv_scale [cap, H/128] fp32 | None)."""
     dev = x.device
     _dev(x, "x", torch.bfloat16)
+    if _rows_of(x, "x", cfg.hidden) < cfg.T:
+        raise ValueError("x has %d rows, needs T = %d" % (x.shape[0], cfg.T))
+    _check_layout(cfg, L, dev)
     if recv is None:
         recv, recv_scale = alloc_recv(cfg, dev)
     fp8 = cfg.payload == PAYLOAD_FP8_E4M3
     _dev(recv, "recv", torch.uint8 if fp8 else torch.bfloat16)
-    sp = _dev(recv_scale, "recv_scale", torch.float32) if fp8 else None
+    rows = _rows_of(recv, "recv", cfg.hidden)
+    sp = None
+    if fp8:
+        sp = _dev(recv_scale, "recv_scale", torch.float32)
+        if _rows_of(recv_scale, "recv_scale", cfg.hidden // 128) < rows:
+            raise ValueError("recv_scale has fewer rows than recv")
+    _same_device(dev, recv=recv, recv_scale=recv_scale if fp8 else None)
     bufs = L.buffers()
-    _check(lib().epl_dispatch(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(), sp,
-                              recv.shape[0] if recv.numel() else 0, _stream(dev)), "epl_dispatch")
+    with torch.cuda.device(dev):
+        _check(lib().epl_dispatch(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(), sp,
+                                  rows if recv.numel() else 0, _stream(dev)), "epl_dispatch")
     return recv, recv_scale
 
 
@@ -192,13 +227,21 @@ def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: 
     """epl_combine: y [>=P, H] bf16, topk_w [T, k] fp32 -> out [T, H] bf16."""
     dev = y.device
     _dev(y, "y", torch.bfloat16)
+    _rows_of(y, "y", cfg.hidden)  # its row count must cover P, which only the device knows
     _dev(topk_w, "topk_w", torch.float32)
+    if _rows_of(topk_w, "topk_w", cfg.topk) < cfg.T:
+        raise ValueError("topk_w has %d rows, needs T = %d" % (topk_w.shape[0], cfg.T))
+    _check_layout(cfg, L, dev)
     if out is None:
         out = torch.empty(max(cfg.T, 1), cfg.hidden, dtype=torch.bfloat16, device=dev)
     _dev(out, "out", torch.bfloat16)
+    if _rows_of(out, "out", cfg.hidden) < cfg.T:
+        raise ValueError("out has %d rows, needs T = %d" % (out.shape[0], cfg.T))
+    _same_device(dev, topk_w=topk_w, out=out)
     bufs = L.buffers()
-    _check(lib().epl_combine(ctypes.byref(cfg), y.data_ptr(), topk_w.data_ptr(), ctypes.byref(bufs), out.data_ptr(),
-                             _stream(dev)), "epl_combine")
+    with torch.cuda.device(dev):
+        _check(lib().epl_combine(ctypes.byref(cfg), y.data_ptr(), topk_w.data_ptr(), ctypes.byref(bufs),
+                                 out.data_ptr(), _stream(dev)), "epl_combine")
     return out
 
 

@@ -166,3 +166,45 @@ def test_other_model_shapes(name, R, E, H, Tr, payload):
     got = bf16_bits(out)
     assert bf16_ulp_distance(got, want).max() <= 1
     assert (got == want).all()
+
+
+def test_binding_rejects_mismatched_tensors():
+    """Tensors that do not match the config are refused on the host, before any launch: a kernel
+    would otherwise read or write past them."""
+    dev = device()
+    R, E, k, Tr, H = 4, 16, 2, 8, 64
+    T = R * Tr
+    idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 21, dev)
+    cfg = epl.config(R, E, k, H, Tr)
+    L = epl.layout(cfg, idx_d)
+    bf = dict(dtype=torch.bfloat16, device=dev)
+    bad_calls = [
+        lambda: epl.layout(cfg, idx_d[:-1]),                                           # T*k - k ids
+        lambda: epl.layout(cfg, idx_d, out=epl.alloc_layout(epl.config(R, E, k, H, Tr + 1), dev)),
+        lambda: epl.dispatch(cfg, torch.zeros(T - 1, H, **bf), L),                     # too few rows of x
+        lambda: epl.dispatch(cfg, torch.zeros(T, H + 8, **bf), L),                     # wrong width
+        lambda: epl.dispatch(cfg, x_d, L, torch.empty(T * k, H + 8, **bf)),            # recv width
+        lambda: epl.dispatch(cfg, x_d, epl.alloc_layout(epl.config(R, E, k, H, Tr + 1), dev)),
+        lambda: epl.combine(cfg, torch.zeros(T * k, H - 8, **bf), w_d, L),             # y width
+        lambda: epl.combine(cfg, torch.zeros(T * k, H, **bf), w_d[:-1], L),            # too few weight rows
+        lambda: epl.combine(cfg, torch.zeros(T * k, H, **bf), torch.zeros(T, k + 1, device=dev), L),
+        lambda: epl.combine(cfg, torch.zeros(T * k, H, **bf), w_d, L, torch.empty(T - 1, H, **bf)),
+    ]
+    for i, call in enumerate(bad_calls):
+        with pytest.raises(ValueError):
+            call()
+            pytest.fail("call %d was accepted" % i)
+    cfg8 = epl.config(R, E, k, 128, Tr, "fp8")
+    L8 = epl.layout(cfg8, idx_d)
+    x8 = torch.zeros(T, 128, **bf)
+    recv8 = torch.empty(T * k, 128, dtype=torch.uint8, device=dev)
+    with pytest.raises(ValueError):
+        epl.dispatch(cfg8, x8, L8, recv8, torch.empty(T * k - 1, 1, dtype=torch.float32, device=dev))
+    torch.cuda.synchronize()
+    # the well-formed calls still work after the refusals
+    recv, _ = epl.dispatch(cfg, x_d, L)
+    out = epl.combine(cfg, recv, w_d, L)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    np.testing.assert_array_equal(bf16_bits(out), oracle.combine(oracle.dispatch_bf16(x, ref.pair_row, ref.P), gw,
+                                                                  ref.pair_row))
