@@ -7,6 +7,7 @@ current HIP stream, and turns status codes into exceptions. There is no fallback
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from dataclasses import dataclass
@@ -147,6 +148,11 @@ def alloc_layout(cfg: Config, device) -> Layout:
                   torch.empty(ws, dtype=torch.uint8, device=device))
 
 
+def _on(dev):
+    """Make dev the current device for a launch, switching only when it is not already."""
+    return contextlib.nullcontext() if torch.cuda.current_device() == dev.index else torch.cuda.device(dev)
+
+
 def _same_device(dev, **tensors) -> None:
     for name, t in tensors.items():
         if t is not None and t.device != dev:
@@ -179,7 +185,7 @@ def layout(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> La
     if L.workspace.numel() < workspace_bytes(cfg):
         raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), workspace_bytes(cfg)))
     bufs = L.buffers()
-    with torch.cuda.device(dev):
+    with _on(dev):
         _check(lib().epl_layout(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs), L.workspace.data_ptr(),
                                 L.workspace.numel(), _stream(dev)), "epl_layout")
     return L
@@ -217,7 +223,7 @@ def dispatch(cfg: Config, x: torch.Tensor, L: Layout, recv: torch.Tensor | None 
             raise ValueError("recv_scale has fewer rows than recv")
     _same_device(dev, recv=recv, recv_scale=recv_scale if fp8 else None)
     bufs = L.buffers()
-    with torch.cuda.device(dev):
+    with _on(dev):
         _check(lib().epl_dispatch(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(), sp,
                                   rows if recv.numel() else 0, _stream(dev)), "epl_dispatch")
     return recv, recv_scale
@@ -239,7 +245,7 @@ def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: 
         raise ValueError("out has %d rows, needs T = %d" % (out.shape[0], cfg.T))
     _same_device(dev, topk_w=topk_w, out=out)
     bufs = L.buffers()
-    with torch.cuda.device(dev):
+    with _on(dev):
         _check(lib().epl_combine(ctypes.byref(cfg), y.data_ptr(), topk_w.data_ptr(), ctypes.byref(bufs),
                                  out.data_ptr(), _stream(dev)), "epl_combine")
     return out

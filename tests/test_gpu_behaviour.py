@@ -208,3 +208,32 @@ def test_binding_rejects_mismatched_tensors():
     ref = oracle.layout(R, E, k, Tr, idx)
     np.testing.assert_array_equal(bf16_bits(out), oracle.combine(oracle.dispatch_bf16(x, ref.pair_row, ref.P), gw,
                                                                   ref.pair_row))
+
+
+def test_two_layers_concurrently_on_two_streams():
+    """The library keeps no state between calls: two different layers enqueued on two streams at
+    once (their kernels may overlap on the GPU) each match the oracle."""
+    dev = device()
+    specs = [(8, 32, 4, 60, 512, 31), (16, 64, 8, 20, 1024, 32)]
+    streams = [torch.cuda.Stream(device=dev) for _ in specs]
+    runs = []
+    for (R, E, k, Tr, H, seed) in specs:
+        idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, seed, dev)
+        runs.append((R, E, k, Tr, H, idx, x, gw, idx_d, x_d, w_d))
+    torch.cuda.synchronize()
+    outs = []
+    for _ in range(3):  # interleave the enqueues of the two layers
+        for (R, E, k, Tr, H, idx, x, gw, idx_d, x_d, w_d), s in zip(runs, streams):
+            with torch.cuda.stream(s):
+                cfg = epl.config(R, E, k, H, Tr)
+                L = epl.layout(cfg, idx_d)
+                recv, _ = epl.dispatch(cfg, x_d, L)
+                outs.append((cfg, L, recv, epl.combine(cfg, recv, w_d, L)))
+    torch.cuda.synchronize()
+    for i, (cfg, L, recv, out) in enumerate(outs):
+        R, E, k, Tr, H, idx, x, gw = runs[i % 2][:8]
+        ref = oracle.layout(R, E, k, Tr, idx)
+        assert_layout_equal(L, ref, "stream %d" % (i % 2))
+        rr = oracle.dispatch_bf16(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), rr)
+        np.testing.assert_array_equal(bf16_bits(out), oracle.combine(rr, gw, ref.pair_row))

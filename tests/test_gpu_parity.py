@@ -225,6 +225,47 @@ def test_combine_parity(R, E, k, Tr, H, seed):
     assert (got == want).all(), "combine within 1 ulp but %d elements not bit-exact" % (got != want).sum()
 
 
+# ---------------------------------------------------------------------- randomised whole layers
+@pytest.mark.parametrize("seed", range(16))
+def test_random_layer_parity(seed):
+    """Random shapes, payloads and routings (duplicates, invalid ids, hot experts) through the whole
+    layer: layout, dispatch (bf16 or fp8) and combine, each compared element by element."""
+    dev = device()
+    rng = np.random.default_rng(900 + seed)
+    R = int(rng.choice([1, 2, 5, 8, 16, 64]))
+    El = int(rng.choice([1, 2, 3, 4]))
+    E = R * El
+    k = int(rng.choice([1, 2, 4, 6, 8, 13]))
+    Tr = int(rng.choice([1, 7, 33, 100]))
+    payload = "fp8" if seed % 2 else "bf16"
+    H = int(rng.choice([128, 384, 1024, 2176])) if payload == "fp8" else int(rng.choice([8, 264, 1032, 2048]))
+    T = R * Tr
+    lo, hi = (-1, E + 1) if seed % 3 else (0, max(1, E // 4))
+    idx = W.with_replacement(seed, T, k, lo, hi).astype(np.int32)
+    x = W.normal_bf16(seed, W.STREAM_X, T * H).reshape(T, H)
+    gw = W.softmax_gate_weights(seed, T, k)
+    w = W.Workload("r", R, E, k, Tr, H, payload, "-")
+    cfg, L = run_layout(w, idx, dev)
+    ref = oracle.layout(R, E, k, Tr, idx)
+    recv, scale = epl.dispatch(cfg, to_dev_bf16(x, dev), L)
+    torch.cuda.synchronize()
+    what = "seed %d: R=%d E=%d k=%d Tr=%d H=%d %s" % (seed, R, E, k, Tr, H, payload)
+    assert_layout_equal(L, ref, what)
+    if payload == "bf16":
+        yh = oracle.dispatch_bf16(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), yh, err_msg=what)
+        y = recv
+    else:
+        q, sc = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(recv[:ref.P].cpu().numpy(), q, err_msg=what)
+        np.testing.assert_array_equal(scale[:ref.P].cpu().numpy().view(np.uint32), sc.view(np.uint32), err_msg=what)
+        yh = W.normal_bf16(seed, W.STREAM_Y, max(ref.P, 1) * H).reshape(-1, H)
+        y = to_dev_bf16(yh, dev)
+    out = epl.combine(cfg, y, torch.from_numpy(gw).to(dev), L)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bf16_bits(out), oracle.combine(yh, gw, ref.pair_row), err_msg=what)
+
+
 # ---------------------------------------------------------------------- extreme hidden sizes
 @pytest.mark.parametrize("H,payload", [(8, "bf16"), (128, "fp8"), (1 << 20, "bf16"), (1 << 20, "fp8")])
 def test_extreme_hidden_sizes(H, payload):
