@@ -181,3 +181,31 @@ def test_binding_rejects_host_tensors_before_any_call():
         epl.layout(cfg_, torch.zeros(6, 2, dtype=torch.int32))
     with pytest.raises(ValueError):
         epl.debug_f32_to_e4m3(torch.zeros(4))
+
+
+from hypothesis import given, settings, strategies as st  # noqa: E402
+
+
+def _valid(R, E, k, H, Tr, payload):
+    """The config rules documented in include/epl.h."""
+    return (R >= 1 and R <= E <= epl.MAX_EXPERTS and E % R == 0 and 1 <= k <= 32 and Tr >= 0 and 8 <= H <= 1 << 20
+            and H % 8 == 0 and R * Tr * k < 2 ** 31 - 1 and payload in (0, 1))
+
+
+@settings(max_examples=400, deadline=None)
+@given(R=st.one_of(st.integers(-2, 70), st.sampled_from([128, 256, 1024, 1025])),
+       E=st.one_of(st.integers(-2, 300), st.sampled_from([512, 1024, 1025, 2048])),
+       k=st.integers(-1, 34), H=st.one_of(st.integers(-8, 300), st.sampled_from([7168, 1 << 20, (1 << 20) + 8])),
+       Tr=st.one_of(st.integers(-2, 5000), st.sampled_from([1 << 20, 1 << 24])), payload=st.integers(-1, 2))
+def test_config_rules_property(lib, R, E, k, H, Tr, payload):
+    """Host-side validation follows the documented rules for any config; rejected configs never
+    reach a launch (the calls below use fake pointers and would fault if they did)."""
+    c = epl.Config(R, E, k, H, Tr, payload)
+    ok = _valid(R, E, k, H, Tr, payload)
+    assert (lib.epl_workspace_bytes(ctypes.byref(c)) > 0) == ok
+    n = lib.epl_layout_launches(ctypes.byref(c))
+    assert (n in (1, 3)) if ok else n == -1
+    if not ok:
+        st_ = call_layout(lib, c)
+        assert st_ in (INVALID, UNSUPPORTED)
+        assert (st_ == UNSUPPORTED) == (payload not in (0, 1) and _valid(R, E, k, H, Tr, 0))
