@@ -5,8 +5,8 @@
 // workgroup stages its tokens' k packed-row indices and k gate weights in LDS with one coalesced
 // load. A wave issues the 16-byte loads of up to 8 expert rows before consuming any (many
 // gathers in flight). It then folds them in the token's own j order, acc = fmaf(w_j, y_j, acc),
-// in fp32 starting from +0, rounds to bf16 (RNE) and stores 16-byte vectors with nontemporal
-// stores (plain stores leave dirty lines whose write-back the next kernel pays for). Pairs with
+// in fp32 starting from +0, rounds to bf16 (RNE) and stores 16-byte vectors with sc1+nt stores
+// (plain stores leave dirty lines whose write-back the next kernel pays for). Pairs with
 // row < 0 (invalid expert id) are skipped.
 #include "epl_internal.h"
 
@@ -56,7 +56,10 @@ __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const 
     u32x4 o;
 #pragma unroll
     for (int i = 0; i < 4; ++i) o[i] = f32x2_to_bf16x2(acc[2 * i], acc[2 * i + 1]);
-    __builtin_nontemporal_store(o, out + g * nv + v);  // streamed: leaves no dirty lines behind
+    // Streamed store through a resource bounded to the output row, device scope (sc1) and
+    // nontemporal: it leaves no dirty lines behind and measured best of the store policies.
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(out + g * nv, 0, nv * 16, kBufferRsrcWord3);
+    __builtin_amdgcn_raw_buffer_store_b128(o, rs, v * 16, 0, kCachePolicySc1Nt);
   }
 }
 
