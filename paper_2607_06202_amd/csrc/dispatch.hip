@@ -23,6 +23,7 @@ constexpr int kWavesPerBlock = kDispatchThreads / kWave;
 // bf16 work unit: one token's columns [u*kBf16Cols, (u+1)*kBf16Cols) in 16-byte vectors.
 constexpr int kBf16VPL = 4;                     // vectors per lane in one unit
 constexpr int kBf16Cols = kWave * kBf16VPL;     // 256 vectors = 4 KiB of a row
+constexpr int64_t kBufferLoadXBytes = 200ll << 20;  // x at least this large: buffer loads (see dispatch_bf16_unit)
 
 // Store one 16-byte vector at vector index v of a row of nv vectors through a buffer resource
 // scoped to that row, with an explicit cache policy. The resource bounds (nv * 16 bytes) also
@@ -40,6 +41,16 @@ __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int
 
 // bf16: unit = (token g, column chunk c). The wave loads its chunk of x[g] once and stores it
 // to the k destination rows, interleaving destinations per vector.
+//
+// BUF_X selects how x is read, both with the default cache policy: buffer loads through a
+// resource bounded to the row, or plain global loads. Measured over three repetitions each
+// (dispatch alone, x rotated):
+// * EP=32 prefill: 3293 -> 3252 us with buffer loads;
+// * EP=256: 380.5 -> 376.3 us with buffer loads;
+// * EP=64 decode: 176.4 -> 178.1 us, slower with buffer loads.
+// The launcher takes buffer loads once x outgrows the 256 MB memory-side cache (decode's x is
+// 117 MB, the others' 235 MB and 1.9 GB).
+template <bool BUF_X>
 __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row,
                                                    u32x4* __restrict__ recv, int64_t g, int c, int k, int nv,
                                                    int64_t cap, int lane) {
@@ -50,8 +61,14 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
   // together; only the stores are guarded. Default cache policy: it measured faster than
   // nontemporal loads here, though x is read once.
   u32x4 buf[kBf16VPL];
+  if constexpr (BUF_X) {
+    const __amdgpu_buffer_rsrc_t xs = __builtin_amdgcn_make_buffer_rsrc(const_cast<u32x4*>(xr), 0, nv * 16, kBufferRsrcWord3);
 #pragma unroll
-  for (int u = 0; u < kBf16VPL; ++u) buf[u] = xr[min(v0 + u * kWave, nv - 1)];
+    for (int u = 0; u < kBf16VPL; ++u) buf[u] = __builtin_amdgcn_raw_buffer_load_b128(xs, min(v0 + u * kWave, nv - 1) * 16, 0, 0);
+  } else {
+#pragma unroll
+    for (int u = 0; u < kBf16VPL; ++u) buf[u] = xr[min(v0 + u * kWave, nv - 1)];
+  }
 #pragma unroll
   for (int u = 0; u < kBf16VPL; ++u) {
     const int v = v0 + u * kWave;
@@ -63,6 +80,7 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
   }
 }
 
+template <bool BUF_X>
 __global__ void __launch_bounds__(kDispatchThreads)
     dispatch_bf16_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
                          int64_t T, int k, int nv, int chunks, int64_t cap) {
@@ -71,7 +89,7 @@ __global__ void __launch_bounds__(kDispatchThreads)
   const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
   for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / chunks;
-    dispatch_bf16_unit(x, pair_row, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
+    dispatch_bf16_unit<BUF_X>(x, pair_row, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
   }
 }
 
@@ -151,8 +169,12 @@ hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* re
   const int chunks = (nv + kBf16Cols - 1) / kBf16Cols;
   const int64_t units = T * chunks;
   const dim3 grid((unsigned)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30));
-  hipLaunchKernelGGL(dispatch_bf16_kernel, grid, dim3(kDispatchThreads), 0, stream, static_cast<const u32x4*>(x),
-                     pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
+  if (T * (int64_t)H * 2 >= kBufferLoadXBytes)
+    hipLaunchKernelGGL(dispatch_bf16_kernel<true>, grid, dim3(kDispatchThreads), 0, stream,
+                       static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
+  else
+    hipLaunchKernelGGL(dispatch_bf16_kernel<false>, grid, dim3(kDispatchThreads), 0, stream,
+                       static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
   return hipGetLastError();
 }
 
