@@ -48,8 +48,8 @@ __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int
 // * EP=32 prefill: 3293 -> 3252 us with buffer loads;
 // * EP=256: 380.5 -> 376.3 us with buffer loads;
 // * EP=64 decode: 176.4 -> 178.1 us, slower with buffer loads.
-// The launcher takes buffer loads once x outgrows the 256 MB memory-side cache (decode's x is
-// 117 MB, the others' 235 MB and 1.9 GB).
+// The launcher takes buffer loads for an x of 200 MB or more, a threshold between decode's 117 MB
+// and the 235 MB and 1.9 GB of the others; why the instruction form matters is not established.
 template <bool BUF_X>
 __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row,
                                                    u32x4* __restrict__ recv, int64_t g, int c, int k, int nv,
