@@ -1,9 +1,9 @@
 #!/usr/bin/env python3
 """Benchmark: one MoE layer's dispatch + combine hot path on one MI355X.
 
-A step is one pass of the whole hot path over one synthetic batch:
-  epl_layout (routing layout) -> epl_dispatch (row scatter) -> epl_combine (gather-reduce),
-with identity experts in between (combine reads the receive buffer). All inputs are resident
+A step is one pass of the whole hot path over one synthetic batch: the routing layout and the row
+scatter (epl_layout_dispatch, or epl_layout then epl_dispatch with --separate), then the
+gather-reduce (epl_combine), with identity experts in between (combine reads the receive buffer). All inputs are resident
 in HBM before timing starts. The token matrix x is read from byte-identical copies in turn, at
 least 512 MB in total, so that no step finds its input in the 256 MB memory-side cache.
 
@@ -54,7 +54,8 @@ def algorithmic_bytes(T, k, H, R, E, P, payload):
 KERNEL_SOURCES = {"route_hist_kernel": "layout.hip", "route_scan_kernel": "layout.hip",
                   "route_finalize_kernel": "layout.hip", "route_single_kernel": "layout.hip",
                   "dispatch_bf16_kernel": "dispatch.hip", "dispatch_fp8_kernel": "dispatch.hip",
-                  "combine_kernel": "combine.hip"}
+                  "combine_kernel": "combine.hip", "fused_bf16_kernel": "dispatch.hip",
+                  "fused_fp8_kernel": "dispatch.hip"}
 
 
 def source_hash(kernel):
@@ -169,6 +170,9 @@ def main():
     ap.add_argument("--workload", default="decode_ep64")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time (0 to skip)")
+    ap.add_argument("--separate", action="store_true",
+                    help="time epl_layout, epl_dispatch and epl_combine as three calls instead of "
+                         "epl_layout_dispatch + epl_combine")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP graph replays of the layer (one graph per x copy) instead of eager launches")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
@@ -176,6 +180,7 @@ def main():
                     help="write profiles/hbm_traffic.json from rocprofv3 --pmc runs (no GPU needed)")
     ap.add_argument("--command", action="append", default=[], help="profiler command recorded with --ingest-counters")
     args = ap.parse_args()
+    args.fused = not args.separate
     if args.ingest_counters:
         ingest_counters(*args.ingest_counters, args.workload, args.command)
         return
@@ -242,12 +247,17 @@ def main():
         y = recv
 
     def step(i, ev=None):
+        # With --fused the layout leg is empty and the dispatch leg is the fused call.
         if ev is not None:
             ev[0].record(stream)
-        epl.layout(cfg, idx_d, out=L)
+        if not args.fused:
+            epl.layout(cfg, idx_d, out=L)
         if ev is not None:
             ev[1].record(stream)
-        epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
+        if args.fused:
+            epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
+        else:
+            epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
         if ev is not None:
             ev[2].record(stream)
         epl.combine(cfg, y, w_d, L, out)
@@ -301,10 +311,14 @@ def main():
             graphs[i % n_x].replay()
             continue
         ev = dev_ev.get(i)
-        epl.layout(cfg, idx_d, out=L)
+        if not args.fused:
+            epl.layout(cfg, idx_d, out=L)
         if ev is not None and dom == "dispatch":
             ev[0].record(stream)
-        epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
+        if args.fused:
+            epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
+        else:
+            epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
         if ev is not None:
             ev[1 if dom == "dispatch" else 0].record(stream)
         epl.combine(cfg, y, w_d, L, out)
@@ -328,8 +342,11 @@ def main():
         dom_us = float(np.mean(per[:, 1 if dom == "dispatch" else 2]))
 
     pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
-    percentiles = {"layout": pct(per[:, 0]), "dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]),
-                   "layer": pct(per.sum(axis=1))}
+    if args.fused:
+        percentiles = {"layout_dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]), "layer": pct(per.sum(axis=1))}
+    else:
+        percentiles = {"layout": pct(per[:, 0]), "dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]),
+                       "layer": pct(per.sum(axis=1))}
 
     nbytes = algorithmic_bytes(w.T, w.k, w.H, w.R, w.E, P, w.payload)
     value = nbytes["total"] / (ms_per_step * 1e-3) / 1e9
@@ -342,6 +359,10 @@ def main():
     achieved = nbytes[dom] / (dom_us * 1e-6) / 1e9
     kname = {"dispatch": "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
              "combine": "combine_kernel"}[dom]
+    launches = epl.layout_dispatch_launches(cfg) if args.fused else None
+    if args.fused and dom == "dispatch":
+        # The events bracket the whole epl_layout_dispatch call, the layout's other kernels included.
+        kname = "epl_layout_dispatch (%d kernels%s)" % (launches, ", finalize fused" if launches == 3 else "")
     roofline = {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": load_traffic(kname, w.name), "algorithmic_bytes": nbytes[dom],
@@ -363,9 +384,14 @@ def main():
         "config": {"workload": w.name, "ranks": w.R, "experts": w.E, "topk": w.k, "tokens_per_rank": w.T // w.R,
                    "hidden": w.H, "payload": w.payload, "routing": w.routing, "pairs": P, "seed": args.seed},
         "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_instrumented": round(us_layer_events, 2),
-        "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2), "us_combine": round(us_combine, 2),
+        "us_layout": None if args.fused else round(us_layout, 2),
+        "us_dispatch": None if args.fused else round(us_dispatch, 2),
+        "us_layout_dispatch": round(us_dispatch + (0.0 if args.fused else us_layout), 2),
+        "us_combine": round(us_combine, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
         "launch": "graph" if graphs is not None else "eager",
+        "calls": "epl_layout_dispatch + epl_combine" if args.fused else "epl_layout + epl_dispatch + epl_combine",
+        "layout_dispatch_launches": launches,
         "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
         "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,
         "roofline": roofline, "x_copies": n_x, "cpu_baseline": cpu,

@@ -134,6 +134,17 @@ epl_status epl_layout(const epl_config *cfg, const int32_t *topk_idx, const epl_
 epl_status epl_dispatch(const epl_config *cfg, const void *x, const epl_layout_buffers *L, void *recv,
                         float *recv_scale, int64_t recv_rows_cap, void *stream);
 
+/* Layout and dispatch in one call: the same outputs as epl_layout followed by epl_dispatch
+ * (Kernel Decomposition: the rows are placed as the tokens are sent). For bf16 payloads with at
+ * most 256 pairs per layout chunk and at most 256 experts, the layout's finalize step (stable
+ * rows, dedup slots) runs inside the dispatch kernel, which saves a launch; other configs run the
+ * layout and then the dispatch (see epl_layout_dispatch_launches). Arguments are those of the two
+ * calls, with the same meaning, alignment and capacity rules; every status those calls can
+ * return is returned before any launch.                                                      */
+epl_status epl_layout_dispatch(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                               void *workspace, size_t workspace_bytes, const void *x, void *recv, float *recv_scale,
+                               int64_t recv_rows_cap, void *stream);
+
 /* Combine: gate-weighted gather-reduce of expert output rows back into token order (the
  * paper's combine: gather expert outputs, restore token order).
  *   y       [>= P rows][H] bf16 expert outputs, row r holds the expert result for packed row r.
@@ -156,6 +167,11 @@ epl_status epl_debug_f32_to_bf16(const float *in, uint16_t *out, int64_t n, void
  * counts it needs; used while T*k <= 16384, Tr*k <= 4096 and its LDS fits in 64 KiB) or 3
  * (histogram, scan, finalize). Returns -1 if cfg is invalid. Host-only, no HIP calls.        */
 int epl_layout_launches(const epl_config *cfg);
+
+/* Kernel launches epl_layout_dispatch issues for cfg: 2 (one-launch layout, dispatch),
+ * 3 (histogram, scan, finalize fused into the dispatch) or 4 (three-launch layout, dispatch).
+ * Returns -1 if cfg is invalid. Host-only, no HIP calls.                                      */
+int epl_layout_dispatch_launches(const epl_config *cfg);
 
 /* Static strings; never NULL. */
 const char *epl_status_str(epl_status status);

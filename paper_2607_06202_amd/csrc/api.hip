@@ -110,6 +110,59 @@ EPL_EXPORT epl_status epl_dispatch(const epl_config* cfg, const void* x, const e
   return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, T, cfg->topk, cfg->hidden, recv_rows_cap, s));
 }
 
+EPL_EXPORT epl_status epl_layout_dispatch(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                          void* workspace, size_t ws_bytes, const void* x, void* recv,
+                                          float* recv_scale, int64_t recv_rows_cap, void* stream) {
+  epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  const bool fp8 = cfg->payload == EPL_PAYLOAD_FP8_E4M3;
+  if (fp8 && cfg->hidden % 128 != 0) return EPL_ERR_UNSUPPORTED;
+  if ((st = check_layout_buffers(L)) != EPL_OK) return st;
+  const epl::Geom g = make_geom(cfg);
+  if (g.T > 0 && (!topk_idx || !x || !recv || (fp8 && !recv_scale))) return EPL_ERR_INVALID_ARG;
+  if (!aligned(topk_idx, 4) || !aligned(x, 16) || !aligned(recv, 16) || (fp8 && !aligned(recv_scale, 4)))
+    return EPL_ERR_ALIGN;
+  if (recv_rows_cap < g.T * cfg->topk) return EPL_ERR_CAPACITY;
+  if (!workspace) return EPL_ERR_WORKSPACE;
+  if (!aligned(workspace, 4)) return EPL_ERR_ALIGN;
+  if (ws_bytes < workspace_bytes(g)) return EPL_ERR_WORKSPACE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* ws = static_cast<int32_t*>(workspace);
+  if (epl::layout_single(g)) {  // small layouts: the one-launch layout, then the dispatch
+    const hipError_t e = epl::launch_layout(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->expert_off, L->rank_off,
+                                            L->seg_off, L->tok_nranks, L->pair_row, L->pair_rslot, L->recv_src,
+                                            L->recv_j, L->num_invalid, s);
+    if (e != hipSuccess) return EPL_ERR_DEVICE;
+    if (fp8)
+      return from_hip(epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden,
+                                               recv_rows_cap, s));
+    return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, recv_rows_cap, s));
+  }
+  if (!epl::fused_dispatch_ok(g, fp8)) {  // three-launch layout, then the dispatch
+    const hipError_t e = epl::launch_layout(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->expert_off, L->rank_off,
+                                            L->seg_off, L->tok_nranks, L->pair_row, L->pair_rslot, L->recv_src,
+                                            L->recv_j, L->num_invalid, s);
+    if (e != hipSuccess) return EPL_ERR_DEVICE;
+    if (fp8)
+      return from_hip(epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden,
+                                               recv_rows_cap, s));
+    return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, recv_rows_cap, s));
+  }
+  const hipError_t e = epl::launch_layout_counts(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->tok_nranks,
+                                                 L->num_invalid, s);
+  if (e != hipSuccess) return EPL_ERR_DEVICE;
+  return from_hip(epl::launch_fused_dispatch(g, topk_idx, ws, L->expert_off, L->rank_off, L->seg_off, L->pair_row,
+                                             L->pair_rslot, L->recv_src, L->recv_j, x, recv, cfg->hidden,
+                                             recv_rows_cap, s));
+}
+
+EPL_EXPORT int epl_layout_dispatch_launches(const epl_config* cfg) {
+  if (check_config(cfg) != EPL_OK) return -1;
+  const epl::Geom g = make_geom(cfg);
+  if (epl::layout_single(g)) return 2;
+  return epl::fused_dispatch_ok(g, cfg->payload == EPL_PAYLOAD_FP8_E4M3) ? 3 : 4;
+}
+
 EPL_EXPORT epl_status epl_combine(const epl_config* cfg, const void* y, const float* topk_w,
                                   const epl_layout_buffers* L, void* out, void* stream) {
   epl_status st = check_config(cfg);

@@ -50,11 +50,11 @@ __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int
 // * EP=64 decode: 176.4 -> 178.1 us, slower with buffer loads.
 // The launcher takes buffer loads for an x of 200 MB or more, a threshold between decode's 117 MB
 // and the 235 MB and 1.9 GB of the others; why the instruction form matters is not established.
-template <bool BUF_X>
-__device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row,
-                                                   u32x4* __restrict__ recv, int64_t g, int c, int k, int nv,
-                                                   int64_t cap, int lane) {
-  const int my_row = lane < k ? pair_row[g * k + lane] : -1;
+// row_of() returns, in lane j < k, the packed row of pair j (-1 if invalid); it is called after the
+// loads of x are issued, so whatever it loads is in flight together with them.
+template <bool BUF_X, class RowFn>
+__device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
+                                                   int64_t g, int c, int k, int nv, int64_t cap, int lane) {
   const u32x4* xr = x + g * nv;
   const int v0 = c * kBf16Cols + lane;
   // Loads are unconditional (index clamped into the row) so that all of them are in flight
@@ -69,6 +69,7 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
 #pragma unroll
     for (int u = 0; u < kBf16VPL; ++u) buf[u] = xr[min(v0 + u * kWave, nv - 1)];
   }
+  const int my_row = row_of();
 #pragma unroll
   for (int u = 0; u < kBf16VPL; ++u) {
     const int v = v0 + u * kWave;
@@ -89,7 +90,8 @@ __global__ void __launch_bounds__(kDispatchThreads)
   const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
   for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / chunks;
-    dispatch_bf16_unit<BUF_X>(x, pair_row, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
+    dispatch_bf16_unit<BUF_X>(
+        x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
   }
 }
 
@@ -97,18 +99,19 @@ __global__ void __launch_bounds__(kDispatchThreads)
 // elements [16l, 16l+16) of the pass: two 16-byte bf16 loads -> one 16-byte E4M3 store per
 // destination. A 128-element block spans 8 lanes, whose max is combined with three
 // xor-shuffles; the first lane of each block stores that block's scale for every destination.
-__device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row,
-                                                  u32x4* __restrict__ recv, float* __restrict__ recv_scale, int64_t g,
-                                                  int p, int k, int H, int64_t cap, int lane) {
+template <class RowFn>
+__device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
+                                                  float* __restrict__ recv_scale, int64_t g, int p, int k, int H,
+                                                  int64_t cap, int lane) {
   const int NB = H / 128;
   const int nvq = H / 16;  // 16-byte fp8 vectors per row
-  const int my_row = lane < k ? pair_row[g * k + lane] : -1;
   const u32x4* xr = x + g * (H / 8);
   const int vq = p * kWave + lane;  // fp8 vector index = element / 16
   const bool on = vq < nvq;         // whole 8-lane blocks are on or off (H % 128 == 0)
   const int vl = min(vq, nvq - 1);  // clamped so the loads need no branch
   u32x4 a = xr[2 * vl];
   u32x4 bv = xr[2 * vl + 1];
+  const int my_row = row_of();
   if (!on) a = bv = u32x4{0, 0, 0, 0};
   float f[16];
 #pragma unroll
@@ -158,7 +161,8 @@ __global__ void __launch_bounds__(kDispatchThreads) __attribute__((amdgpu_waves_
   const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
   for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / npass;
-    dispatch_fp8_unit(x, pair_row, recv, recv_scale, g, (int)(u - g * npass), k, H, cap, lane);
+    dispatch_fp8_unit(x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, recv_scale, g,
+                      (int)(u - g * npass), k, H, cap, lane);
   }
 }
 
@@ -186,6 +190,220 @@ hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* rec
   const dim3 grid((unsigned)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30));
   hipLaunchKernelGGL(dispatch_fp8_kernel, grid, dim3(kDispatchThreads), 0, stream, static_cast<const u32x4*>(x),
                      pair_row, static_cast<u32x4*>(recv), recv_scale, T, k, H, npass, cap);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------ layout finalize fused into dispatch
+// epl_layout_dispatch runs K1 and K2 of the layout, then one kernel that does both the layout's
+// finalize step and the dispatch. No workgroup waits on another; each dispatch wave works out the
+// rows of its own token from what K1 and K2 left in the workspace, with exactly the definitions
+// route_finalize_kernel applies to a whole chunk:
+// * row of pair (g, j) = first row of its expert (exclusive prefix of recv_cnt)
+//                      + rows of the expert before the token's chunk (K2's chunk offsets)
+//                      + earlier pairs of the chunk with the same expert (an LDS histogram of the
+//                        chunk's earlier tokens plus a ballot match over the token's own choices);
+// * slot of a first pair = slots of its rank before the chunk (K2) + earlier first pairs of the
+//   chunk bound for that rank; other valid pairs share the slot of their token's first pair on
+//   the same rank.
+// The wave of column chunk 0 also writes the token's pair_row, pair_rslot, recv_src and recv_j.
+// A few extra workgroups at the end of the grid write expert_off, rank_off and seg_off. The loads
+// of x are issued before the row computation, so they are in flight while it runs.
+struct FusedLayout {
+  Geom G;
+  const int32_t* idx;
+  const int32_t* chunk_e;   // [E][nblk] rows of each expert before each chunk (K2)
+  const int32_t* chunk_r;   // [nblk][R] slots of each rank before each chunk (K2)
+  const int32_t* recv_cnt;  // [E]
+  const int32_t* seg_rel;   // [E][R]
+  const uint32_t* fmask;    // [T] first-pair bitmask of each token (K1)
+  int32_t* expert_off;
+  int32_t* rank_off;
+  int32_t* seg_off;
+  int32_t* pair_row;
+  int32_t* pair_rslot;
+  int32_t* recv_src;
+  int32_t* recv_j;
+};
+
+// Sizes the fused kernel is built for: at most kFusedSlots * 64 pairs per chunk (CT * k) and
+// kFusedPer * 64 experts. hist is this wave's LDS [E + R].
+constexpr int kFusedSlots = 4;
+constexpr int kFusedPer = 4;
+__device__ __forceinline__ int token_rows(const FusedLayout& F, int64_t g, bool meta, int32_t* hist, int lane) {
+  const Geom& G = F.G;
+  const int k = G.k;
+  const int s = (int)(g / G.Tr);
+  const int t = (int)(g - (int64_t)s * G.Tr);
+  const int c = t / G.CT;
+  const int b = s * G.NC + c;
+  const int64_t tok0 = (int64_t)s * G.Tr + (int64_t)c * G.CT;  // first token of the chunk
+  const int nb = (int)(g - tok0) * k;                            // earlier pairs of the chunk, < CT * k
+  const int64_t cb = tok0 * k;
+
+  // Every independent load first (indices clamped, so none sits behind a branch).
+  const bool mine = lane < k;
+  const int e = F.idx[g * k + min(lane, k - 1)];
+  const uint32_t fm = F.fmask[g];
+  const int per = (G.E + kWave - 1) / kWave;  // experts per lane in the prefix of recv_cnt, <= kFusedPer
+  int rc[kFusedPer];
+#pragma unroll
+  for (int i = 0; i < kFusedPer; ++i) rc[i] = F.recv_cnt[min(lane * per + i, G.E - 1)];
+  int ep[kFusedSlots];
+  uint32_t fp[kFusedSlots];
+#pragma unroll
+  for (int q = 0; q < kFusedSlots; ++q) {
+    const int i = min(q * kWave + lane, max(nb - 1, 0));
+    ep[q] = nb > 0 ? F.idx[cb + i] : -1;
+    fp[q] = nb > 0 ? F.fmask[tok0 + small_div(i, G.inv_k)] : 0u;
+  }
+  const bool valid = mine && (unsigned)e < (unsigned)G.E;
+  const int ev = valid ? e : 0;
+  const int d = valid ? small_div(e, G.inv_El) : 0;
+  const int base_e = F.chunk_e[(int64_t)ev * G.nblk + b];
+  const int base_r = F.chunk_r[(int64_t)b * G.R + d];
+
+  // Histograms of the chunk's earlier pairs: experts, and ranks of first pairs.
+  int32_t* he = hist;
+  int32_t* hr = hist + G.E;
+  for (int i = lane; i < G.E + G.R; i += kWave) hist[i] = 0;
+#pragma unroll
+  for (int q = 0; q < kFusedSlots; ++q) {
+    const int i = q * kWave + lane;
+    const int xe = ep[q];
+    if (i < nb && (unsigned)xe < (unsigned)G.E) {
+      atomicAdd(&he[xe], 1);
+      const int tp = small_div(i, G.inv_k);
+      if ((fp[q] >> (i - tp * k)) & 1u) atomicAdd(&hr[small_div(xe, G.inv_El)], 1);
+    }
+  }
+
+  // First row of each expert: exclusive prefix of recv_cnt. Lane L holds experts
+  // [L*per, L*per + per); the prefix at expert ev comes from lane ev / per.
+  int run = 0;
+  int ps[kFusedPer];
+#pragma unroll
+  for (int i = 0; i < kFusedPer; ++i) {
+    run += (i < per && lane * per + i < G.E) ? rc[i] : 0;
+    ps[i] = run;
+  }
+  const int incl = wave_inclusive_sum(run);
+  const int P = __shfl(incl, kWave - 1, kWave);  // valid pairs in the whole layout
+  const int L = ev / per;
+  const int il = ev - L * per;
+  int eoff = __shfl(incl - run, L, kWave);
+#pragma unroll
+  for (int i = 0; i + 1 < kFusedPer; ++i) {
+    if (i + 1 >= per) break;  // wave-uniform
+    const int v = __shfl(ps[i], L, kWave);
+    if (i == il - 1) eoff += v;
+  }
+
+  const int rank_e = he[ev] + rank_in_mask(match_key(valid, ev, G.ebits));
+  const bool first = valid && ((fm >> min(lane, 31)) & 1u);
+  const int row = valid ? eoff + base_e + rank_e : -1;
+  const int slot = first ? base_r + hr[d] : -1;
+  // The token's first pair on a rank is its lowest valid lane with that rank.
+  const uint64_t md = match_key(valid, d, G.rbits);
+  const int lead = valid ? (int)__builtin_ctzll(md) : 0;
+  const int rslot = __shfl(slot, lead, kWave);
+  if (meta && mine) {
+    F.pair_row[g * k + lane] = row;
+    F.pair_rslot[g * k + lane] = valid ? rslot : -1;
+    if (valid && row < P) {  // always true for a consistent layout; keeps stores in bounds
+      F.recv_src[row] = (int32_t)g;
+      F.recv_j[row] = lane;
+    }
+  }
+  return mine ? row : -1;
+}
+
+// Workgroups past the dispatch units: expert_off and rank_off (the first of them) and one slice
+// of seg_off each. lds holds at least E + 1 ints.
+__device__ __forceinline__ void fused_meta_block(const FusedLayout& F, int m, int nmeta, int32_t* lds) {
+  static_assert(kDispatchThreads == kLayoutThreads, "block_exclusive_sum assumes layout-sized workgroups");
+  __shared__ int32_t scratch[kLayoutWaves];
+  const Geom& G = F.G;
+  const int tid = threadIdx.x;
+  int32_t* eoff = lds;
+  const int per = (G.E + kLayoutThreads - 1) / kLayoutThreads;
+  const int e0 = min(G.E, tid * per), e1 = min(G.E, e0 + per);
+  int rc[kLayoutSlots];
+#pragma unroll
+  for (int q = 0; q < kLayoutSlots; ++q) rc[q] = F.recv_cnt[min(e0 + q, G.E - 1)];
+  int sum = 0;
+#pragma unroll
+  for (int q = 0; q < kLayoutSlots; ++q) sum += e0 + q < e1 ? rc[q] : 0;
+  int total;
+  int run = block_exclusive_sum(sum, total, scratch);  // synchronises the workgroup
+#pragma unroll
+  for (int q = 0; q < kLayoutSlots; ++q) {
+    if (e0 + q >= e1) break;
+    eoff[e0 + q] = run;
+    run += rc[q];
+  }
+  if (tid == 0) eoff[G.E] = total;
+  __syncthreads();
+  if (m == 0) {
+    for (int e = tid; e <= G.E; e += kLayoutThreads) F.expert_off[e] = eoff[e];
+    for (int r = tid; r <= G.R; r += kLayoutThreads) F.rank_off[r] = eoff[r * G.El];
+  }
+  const int nseg = G.E * G.R;
+  const int seg_per = (nseg + nmeta - 1) / nmeta;
+  const int i1 = min(nseg, (m + 1) * seg_per);
+  for (int i = m * seg_per + tid; i < i1; i += kLayoutThreads)
+    F.seg_off[i] = eoff[small_div(i, G.inv_R)] + F.seg_rel[i];
+}
+
+template <bool BUF_X>
+__global__ void __launch_bounds__(kDispatchThreads)
+    fused_bf16_kernel(FusedLayout F, const u32x4* __restrict__ x, u32x4* __restrict__ recv, int nv, int chunks,
+                      int64_t cap, int unit_grid, int nmeta) {
+  extern __shared__ int32_t lds[];
+  if ((int)blockIdx.x >= unit_grid) {
+    fused_meta_block(F, (int)blockIdx.x - unit_grid, nmeta, lds);
+    return;
+  }
+  const int lane = threadIdx.x % kWave;
+  const int w = threadIdx.x / kWave;
+  int32_t* hist = lds + w * (F.G.E + F.G.R);
+  const int64_t units = F.G.T * chunks;
+  const int64_t stride = (int64_t)unit_grid * kWavesPerBlock;
+  for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + w; u < units; u += stride) {
+    const int64_t g = u / chunks;
+    const int c = (int)(u - g * chunks);
+    dispatch_bf16_unit<BUF_X>(x, [&] { return token_rows(F, g, c == 0, hist, lane); }, recv, g, c, F.G.k, nv, cap,
+                              lane);
+  }
+}
+
+bool fused_dispatch_ok(const Geom& g, bool fp8) {
+  return !fp8 && g.CT * g.k <= kFusedSlots * kWave && g.E <= kFusedPer * kWave;
+}
+
+hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* expert_off,
+                                 int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
+                                 int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int64_t cap,
+                                 hipStream_t stream) {
+  const WsLayout wl = ws_layout(g);
+  const FusedLayout F{g,          idx,          ws + wl.chunk_e, ws + wl.chunk_r,
+                      ws + wl.recv_cnt, ws + wl.seg_rel, reinterpret_cast<const uint32_t*>(ws + wl.fmask),
+                      expert_off, rank_off,     seg_off,         pair_row,
+                      pair_rslot, recv_src,     recv_j};
+  const int nmeta = (int)std::max<int64_t>(1, ((int64_t)g.E * g.R + 4 * kDispatchThreads - 1) / (4 * kDispatchThreads));
+  const int chunks = (H / 8 + kBf16Cols - 1) / kBf16Cols;
+  const int64_t units = g.T * chunks;
+  const int unit_grid = (int)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30);
+  const dim3 grid((unsigned)(unit_grid + nmeta));
+  const size_t lds = sizeof(int32_t) * std::max<size_t>((size_t)kWavesPerBlock * (g.E + g.R), (size_t)g.E + 1);
+  const bool buf_x = g.T * (int64_t)H * 2 >= kBufferLoadXBytes;
+  const u32x4* xv = static_cast<const u32x4*>(x);
+  u32x4* rv = static_cast<u32x4*>(recv);
+  if (buf_x)
+    hipLaunchKernelGGL(fused_bf16_kernel<true>, grid, dim3(kDispatchThreads), lds, stream, F, xv, rv, H / 8, chunks,
+                       cap, unit_grid, nmeta);
+  else
+    hipLaunchKernelGGL(fused_bf16_kernel<false>, grid, dim3(kDispatchThreads), lds, stream, F, xv, rv, H / 8, chunks,
+                       cap, unit_grid, nmeta);
   return hipGetLastError();
 }
 

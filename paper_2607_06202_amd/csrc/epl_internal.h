@@ -77,6 +77,12 @@ inline WsLayout ws_layout(const Geom& g) {
   return w;
 }
 
+// Small integer quotient q = n / d for 0 <= n < 2^21 and the float reciprocal inv_d = 1/d:
+// q = (int)((n + 0.5f) * inv_d). The exact quotient sits at least 0.5/d away from an integer, and
+// two float roundings perturb (n + 0.5)/d by at most (n + 0.5) * 2^-22 / d, which is smaller than
+// 0.5/d. So the truncated result is exact.
+__device__ __forceinline__ int small_div(int n, float inv_d) { return (int)(((float)n + 0.5f) * inv_d); }
+
 // ---------------------------------------------------------------- wave64 primitives
 __device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0)); }
 
@@ -161,6 +167,10 @@ __device__ __forceinline__ float bf16hi_to_f32(uint32_t w) { return __uint_as_fl
 // ---------------------------------------------------------------- launchers (host side)
 size_t single_lds_bytes(const Geom& g);
 bool layout_single(const Geom& g);  // true if epl_layout runs as one launch for this geometry
+// K1 and K2 only: histograms, dedup masks and the prefix scans, left in the workspace for a
+// finalize step (route_finalize_kernel, or the fused finalize in the dispatch kernels).
+hipError_t launch_layout_counts(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
+                                int32_t* tok_nranks, int32_t* num_invalid, hipStream_t stream);
 hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
                          int32_t* expert_off, int32_t* rank_off, int32_t* seg_off, int32_t* tok_nranks,
                          int32_t* pair_row, int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j,
@@ -170,6 +180,13 @@ hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* re
                                 int64_t cap, hipStream_t stream);
 hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* recv, float* recv_scale, int64_t T,
                                int k, int H, int64_t cap, hipStream_t stream);
+// The layout's finalize step fused into the bf16 dispatch (after launch_layout_counts on the same
+// stream), for the geometries fused_dispatch_ok accepts.
+bool fused_dispatch_ok(const Geom& g, bool fp8);
+hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* expert_off,
+                                 int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
+                                 int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int64_t cap,
+                                 hipStream_t stream);
 hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
                           int H, hipStream_t stream);
 

@@ -23,15 +23,11 @@
 //                      prefix then yields pair_row, recv_src, recv_j and pair_rslot.
 //
 // Small integer quotients (pair -> token within a chunk, expert -> rank, seg_off index -> expert;
-// every numerator < 2^21) use
-// q = (int)((n + 0.5f) * (1.0f / d)). The exact quotient sits at least 0.5/d away from an
-// integer, and two float roundings perturb (n + 0.5)/d by at most (n + 0.5) * 2^-22 / d, which is
-// smaller than 0.5/d. So the truncated result is exact.
+// every numerator < 2^21) use small_div, which is exact in that range.
 #include "epl_internal.h"
 
 namespace epl {
 
-__device__ __forceinline__ int small_div(int n, float inv_d) { return (int)(((float)n + 0.5f) * inv_d); }
 
 // Dedup of one token: bit j is set if pair j is valid (dt[j] >= 0) and no earlier valid pair of
 // the token targets the same destination rank dt[j].
@@ -661,6 +657,18 @@ hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t
                        recv_j, num_invalid);
     return hipGetLastError();
   }
+  hipError_t err = launch_layout_counts(g, idx, ws, send_cnt, rank_cnt, tok_nranks, num_invalid, stream);
+  if (err != hipSuccess) return err;
+  const WsLayout wl = ws_layout(g);
+  hipLaunchKernelGGL(route_finalize_kernel, dim3(g.nblk), dim3(kLayoutThreads), finalize_lds_bytes(g), stream, g,
+                     idx, ws + wl.chunk_e, ws + wl.chunk_r, ws + wl.recv_cnt, ws + wl.seg_rel,
+                     reinterpret_cast<const uint32_t*>(ws + wl.fmask), expert_off, rank_off, seg_off, pair_row,
+                     pair_rslot, recv_src, recv_j);
+  return hipGetLastError();
+}
+
+hipError_t launch_layout_counts(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
+                                int32_t* tok_nranks, int32_t* num_invalid, hipStream_t stream) {
   const WsLayout wl = ws_layout(g);
   int32_t* chunk_e = ws + wl.chunk_e;
   int32_t* chunk_r = ws + wl.chunk_r;
@@ -677,12 +685,6 @@ hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t
 
   hipLaunchKernelGGL(route_scan_kernel, dim3(g.E + g.R + 1), dim3(kLayoutThreads), 0, stream, g, chunk_e, chunk_r,
                      inval, recv_cnt, send_cnt, rank_cnt, seg_rel, num_invalid);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
-
-  hipLaunchKernelGGL(route_finalize_kernel, dim3(g.nblk), dim3(kLayoutThreads), finalize_lds_bytes(g), stream, g,
-                     idx, chunk_e, chunk_r, recv_cnt, seg_rel, fmask, expert_off, rank_off, seg_off, pair_row,
-                     pair_rslot, recv_src, recv_j);
   return hipGetLastError();
 }
 

@@ -85,6 +85,10 @@ def lib() -> ctypes.CDLL:
         L.epl_status_str.argtypes = [ctypes.c_int]
         L.epl_version.restype = ctypes.c_char_p
         L.epl_version.argtypes = []
+        L.epl_layout_dispatch.restype = ctypes.c_int
+        L.epl_layout_dispatch.argtypes = [CP, P, LP, P, S, P, P, P, I64, P]
+        L.epl_layout_dispatch_launches.restype = ctypes.c_int
+        L.epl_layout_dispatch_launches.argtypes = [CP]
         L.epl_layout_launches.restype = ctypes.c_int
         L.epl_layout_launches.argtypes = [CP]
         _lib = L
@@ -229,6 +233,39 @@ def dispatch(cfg: Config, x: torch.Tensor, L: Layout, recv: torch.Tensor | None 
     return recv, recv_scale
 
 
+def layout_dispatch(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: Layout | None = None,
+                    recv: torch.Tensor | None = None, recv_scale: torch.Tensor | None = None):
+    """epl_layout_dispatch: layout and dispatch in one call -> (Layout, recv, recv_scale | None)."""
+    dev = topk_idx.device
+    _dev(topk_idx, "topk_idx", torch.int32)
+    if topk_idx.numel() != cfg.T * cfg.topk:
+        raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
+    _dev(x, "x", torch.bfloat16)
+    if _rows_of(x, "x", cfg.hidden) < cfg.T:
+        raise ValueError("x has %d rows, needs T = %d" % (x.shape[0], cfg.T))
+    L = out if out is not None else alloc_layout(cfg, dev)
+    _check_layout(cfg, L, dev)
+    if L.workspace.numel() < workspace_bytes(cfg):
+        raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), workspace_bytes(cfg)))
+    if recv is None:
+        recv, recv_scale = alloc_recv(cfg, dev)
+    fp8 = cfg.payload == PAYLOAD_FP8_E4M3
+    _dev(recv, "recv", torch.uint8 if fp8 else torch.bfloat16)
+    rows = _rows_of(recv, "recv", cfg.hidden)
+    sp = None
+    if fp8:
+        sp = _dev(recv_scale, "recv_scale", torch.float32)
+        if _rows_of(recv_scale, "recv_scale", cfg.hidden // 128) < rows:
+            raise ValueError("recv_scale has fewer rows than recv")
+    _same_device(dev, x=x, recv=recv, recv_scale=recv_scale if fp8 else None)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_layout_dispatch(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                         L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
+                                         sp, rows if recv.numel() else 0, _stream(dev)), "epl_layout_dispatch")
+    return L, recv, recv_scale
+
+
 def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):
     """epl_combine: y [>=P, H] bf16, topk_w [T, k] fp32 -> out [T, H] bf16."""
     dev = y.device
@@ -272,6 +309,14 @@ def layout_launches(cfg: Config) -> int:
     n = lib().epl_layout_launches(ctypes.byref(cfg))
     if n < 0:
         raise EplError(1, "epl_layout_launches")
+    return n
+
+
+def layout_dispatch_launches(cfg: Config) -> int:
+    """Kernel launches epl_layout_dispatch issues for cfg: 2, 3 (finalize fused into dispatch) or 4."""
+    n = lib().epl_layout_dispatch_launches(ctypes.byref(cfg))
+    if n < 0:
+        raise EplError(1, "epl_layout_dispatch_launches")
     return n
 
 

@@ -73,7 +73,8 @@ struct Case {
   epl_payload payload;
 };
 
-bool run_case(const Case& c, uint64_t seed, hipStream_t stream) {
+// With fused, layout and dispatch run as one epl_layout_dispatch call.
+bool run_case(const Case& c, uint64_t seed, hipStream_t stream, bool fused) {
   const int64_t T = (int64_t)c.R * c.Tr, Tk = T * c.k;
   const bool fp8 = c.payload == EPL_PAYLOAD_FP8_E4M3;
   std::vector<int32_t> idx(Tk);
@@ -121,9 +122,10 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream) {
   uint16_t* d_o = nullptr;
   HIP_OK(hipMalloc(&d_o, (size_t)std::max<int64_t>(T, 1) * c.H * 2));
 
-  bool ok = epl_layout(&cfg, d_idx, &L, ws, ws_bytes, stream) == EPL_OK &&
-            epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk, stream) == EPL_OK &&
-            epl_combine(&cfg, d_y, d_w, &L, d_o, stream) == EPL_OK;
+  bool ok = fused ? epl_layout_dispatch(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk, stream) == EPL_OK
+                  : (epl_layout(&cfg, d_idx, &L, ws, ws_bytes, stream) == EPL_OK &&
+                     epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk, stream) == EPL_OK);
+  ok = ok && epl_combine(&cfg, d_y, d_w, &L, d_o, stream) == EPL_OK;
   if (!ok) std::printf("a call returned an error status\n");
   HIP_OK(hipStreamSynchronize(stream));
 
@@ -158,6 +160,10 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream) {
          epl_layout(&cfg, d_idx, &L, ws, ws_bytes - 4, stream) == EPL_ERR_WORKSPACE &&
          epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk - 1, stream) == EPL_ERR_CAPACITY &&
          epl_dispatch(&cfg, d_x, &L, (char*)d_recv + 2, d_scale, Tk, stream) == EPL_ERR_ALIGN &&
+         epl_layout_dispatch(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk - 1, stream) ==
+             EPL_ERR_CAPACITY &&
+         epl_layout_dispatch(&cfg, d_idx, &L, ws, ws_bytes - 4, d_x, d_recv, d_scale, Tk, stream) ==
+             EPL_ERR_WORKSPACE &&
          epl_combine(&cfg, d_y, d_w, &L, (char*)d_o + 8, stream) == EPL_ERR_ALIGN;
     if (!ok) std::printf("an invalid call was not rejected with the documented status\n");
   }
@@ -171,8 +177,9 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream) {
   HIP_OK(hipFree(d_recv));
   if (d_scale) HIP_OK(hipFree(d_scale));
   HIP_OK(hipFree(d_o));
-  std::printf("case R=%d E=%d k=%d Tr=%d H=%d %s layout launches=%d: %s\n", c.R, c.E, c.k, c.Tr, c.H,
-              fp8 ? "fp8" : "bf16", epl_layout_launches(&cfg), ok ? "ok" : "FAILED");
+  std::printf("case R=%d E=%d k=%d Tr=%d H=%d %s %s (%d launches): %s\n", c.R, c.E, c.k, c.Tr, c.H,
+              fp8 ? "fp8" : "bf16", fused ? "epl_layout_dispatch" : "epl_layout + epl_dispatch",
+              fused ? epl_layout_dispatch_launches(&cfg) : epl_layout_launches(&cfg) + 1, ok ? "ok" : "FAILED");
   return ok;
 }
 
@@ -190,7 +197,11 @@ int main() {
   };
   bool ok = true;
   uint64_t seed = 12345;
-  for (const Case& c : cases) ok = run_case(c, seed++, stream) && ok;
+  for (const Case& c : cases) {
+    ok = run_case(c, seed, stream, false) && ok;
+    ok = run_case(c, seed, stream, true) && ok;
+    ++seed;
+  }
   HIP_OK(hipStreamDestroy(stream));
   if (!ok) return 1;
   std::printf("c abi check ok\n");

@@ -59,6 +59,20 @@ def test_layout_launch_count():
         epl.layout_launches(epl.config(3, 16, 8, 64, 4))                 # E % R != 0
 
 
+def test_layout_dispatch_launch_count():
+    """The finalize step runs inside the dispatch for bf16 with at most 256 pairs per chunk and 256
+    experts (3 launches); small layouts take 2, everything else 4."""
+    want = {"tiny": 2, "decode_ep64": 3, "prefill_ep32": 4, "skewed_fp8_ep64": 4, "large_ep256": 4}
+    for name, n in want.items():
+        w = W.WORKLOADS[name]
+        assert epl.layout_dispatch_launches(epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)) == n, name
+    assert epl.layout_dispatch_launches(epl.config(64, 256, 8, 7168, 128, "fp8")) == 4  # decode shape, fp8
+    assert epl.layout_dispatch_launches(epl.config(64, 512, 8, 7168, 128)) == 4         # 512 experts
+    assert epl.layout_dispatch_launches(epl.config(64, 256, 8, 7168, 130)) == 4         # 264 pairs per chunk
+    with pytest.raises(epl.EplError):
+        epl.layout_dispatch_launches(epl.config(3, 16, 8, 64, 4))
+
+
 def test_version_and_status_strings(lib):
     assert "gfx950" in epl.version()
     for code in range(7):

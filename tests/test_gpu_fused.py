@@ -1,0 +1,99 @@
+"""epl_layout_dispatch against the CPU oracle: every layout output and the bf16 / fp8 payload, bit for
+bit. It takes three paths, and every case asserts which one it exercises:
+* 3 launches, the layout's finalize step fused into the bf16 dispatch (at most 256 pairs per
+  chunk and 256 experts): ragged last chunks, duplicates, invalid ids, 1 and 2 experts per rank,
+  more choices than experts;
+* 4 launches, the layout then the dispatch (larger chunks, more experts, fp8);
+* 2 launches for small layouts."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_06202_amd import epl
+from paper_2607_06202_amd import workloads as W
+from tests.gpu_util import assert_layout_equal, bf16_bits, device, to_dev_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(R, E, k, Tr, H, payload, seed, idx=None):
+    dev = device()
+    T = R * Tr
+    if idx is None:
+        idx = W.with_replacement(seed, T, k, -1, E + 1).astype(np.int32)
+    x = W.normal_bf16(seed, W.STREAM_X, T * H).reshape(T, H)
+    cfg = epl.config(R, E, k, H, Tr, payload)
+    L, recv, sc = epl.layout_dispatch(cfg, torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev))
+    torch.cuda.synchronize()
+    what = "R=%d E=%d k=%d Tr=%d H=%d %s" % (R, E, k, Tr, H, payload)
+    ref = oracle.layout(R, E, k, Tr, idx)
+    assert_layout_equal(L, ref, what)
+    if payload == "bf16":
+        np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), oracle.dispatch_bf16(x, ref.pair_row, ref.P),
+                                      err_msg=what)
+    else:
+        q, s = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(recv[:ref.P].cpu().numpy(), q, err_msg=what)
+        np.testing.assert_array_equal(sc[:ref.P].cpu().numpy().view(np.uint32), s.view(np.uint32), err_msg=what)
+    return cfg, L, ref
+
+
+@pytest.mark.parametrize("R,E,k,Tr,H,seed,launches", [
+    (64, 256, 8, 40, 1024, 0, 3),    # chunks of 10 tokens (80 pairs)
+    (32, 256, 8, 130, 512, 1, 3),    # chunks of 17 tokens, ragged last chunk
+    (128, 256, 4, 50, 2048, 2, 3),   # two experts per rank
+    (256, 256, 8, 16, 520, 3, 3),    # one expert per rank
+    (2, 4, 5, 2000, 64, 4, 3),       # more choices than experts
+    (64, 256, 8, 100, 8, 5, 3),      # 200 pairs per chunk; one 16-byte vector per row
+    (16, 64, 8, 1024, 64, 6, 4),     # 512 pairs per chunk
+    (8, 1024, 32, 1024, 64, 7, 4),   # k = 32, E = 1024
+])
+def test_layout_dispatch_bf16(R, E, k, Tr, H, seed, launches):
+    cfg, _, _ = _check(R, E, k, Tr, H, "bf16", seed)
+    assert epl.layout_dispatch_launches(cfg) == launches
+
+
+@pytest.mark.parametrize("R,E,k,Tr,H,seed", [(64, 256, 8, 40, 1024, 10), (16, 160, 8, 257, 1152, 11)])
+def test_layout_dispatch_fp8(R, E, k, Tr, H, seed):
+    cfg, _, _ = _check(R, E, k, Tr, H, "fp8", seed)
+    assert epl.layout_dispatch_launches(cfg) == 4
+
+
+def test_layout_dispatch_small_layout():
+    cfg, _, _ = _check(4, 16, 2, 128, 256, "bf16", 20)
+    assert epl.layout_dispatch_launches(cfg) == 2
+
+
+def test_layout_dispatch_all_invalid_and_empty():
+    cfg, _, _ = _check(64, 256, 8, 40, 128, "bf16", 30, idx=np.full((64 * 40, 8), -1, np.int32))
+    assert epl.layout_dispatch_launches(cfg) == 3
+    _check(64, 256, 8, 0, 128, "bf16", 31, idx=np.zeros((0, 8), np.int32))
+
+
+@pytest.mark.parametrize("name", ["decode_ep64", "skewed_fp8_ep64", "large_ep256", "prefill_ep32"])
+def test_layout_dispatch_matches_separate_calls_at_full_size(name):
+    """The named workloads in the benchmark's configuration: the fused call and epl_layout then
+    epl_dispatch give identical layouts and identical payloads (compared on the device)."""
+    dev = device()
+    w = W.WORKLOADS[name]
+    idx_d = torch.from_numpy(W.routing(w)).to(dev)
+    x_d = W.device_normal_bf16((w.T, w.H), seed=3, device=dev)
+    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)
+    L1 = epl.layout(cfg, idx_d)
+    r1, s1 = epl.dispatch(cfg, x_d, L1)
+    torch.cuda.synchronize()
+    P = int(L1.expert_off[-1])
+    r1p = r1[:P].clone()
+    s1p = None if s1 is None else s1[:P].clone()
+    del r1, s1
+    L2, r2, s2 = epl.layout_dispatch(cfg, idx_d, x_d)
+    torch.cuda.synchronize()
+    for n, _ in epl.LayoutBuffers._fields_:
+        a, b = getattr(L1, n), getattr(L2, n)
+        if n in ("recv_src", "recv_j"):
+            a, b = a[:P], b[:P]
+        assert torch.equal(a, b), "%s: %s differs" % (name, n)
+    assert torch.equal(r1p.view(torch.uint8), r2[:P].view(torch.uint8)), name
+    if s1p is not None:
+        assert torch.equal(s1p.view(torch.int32), s2[:P].view(torch.int32)), name
