@@ -3,8 +3,10 @@
 
 A step is one pass of the whole hot path over one synthetic batch: the routing layout and the row
 scatter (epl_layout_dispatch, or epl_layout then epl_dispatch with --separate), then the
-gather-reduce (epl_combine), with identity experts in between (combine reads the receive buffer). All inputs are resident
-in HBM before timing starts. The token matrix x is read from byte-identical copies in turn, at
+gather-reduce (epl_combine), with identity experts in between (combine reads the receive buffer).
+Steps that carry timing events issue epl_layout_dispatch as its two phases, epl_layout_counts then
+epl_dispatch_rows (the same kernels), so that the row kernel is timed on its own. All inputs are
+resident in HBM before timing starts. The token matrix x is read from byte-identical copies in turn, at
 least 512 MB in total, so that no step finds its input in the 256 MB memory-side cache.
 
 Default workload: EP=64 decode. 64 virtual ranks, 256 experts (4 per rank), top-8, 128
@@ -45,8 +47,10 @@ def algorithmic_bytes(T, k, H, R, E, P, payload):
     b = 1 if payload == "fp8" else 2
     dispatch = T * H * 2 + T * k * 4 + P * H * b + (P * NB * 4 if payload == "fp8" else 0)
     combine = P * H * 2 + 2 * T * k * 4 + T * H * 2
-    layout = T * k * 4 + 4 * (R * E + R * R + (E + 1) + (R + 1) + E * R + T + 2 * T * k + 2 * P + 1)
-    return {"layout": layout, "dispatch": dispatch, "combine": combine,
+    placement = 4 * ((E + 1) + (R + 1) + E * R + 2 * T * k + 2 * P)  # offsets, pair rows/slots, recv_src/j
+    layout = T * k * 4 + 4 * (R * E + R * R + T + 1) + placement
+    # The row kernel with the layout's finalize step fused in also writes the placement metadata.
+    return {"layout": layout, "dispatch": dispatch, "combine": combine, "rows_fused": dispatch + placement,
             "total": layout + dispatch + combine}
 
 
@@ -54,8 +58,7 @@ def algorithmic_bytes(T, k, H, R, E, P, payload):
 KERNEL_SOURCES = {"route_hist_kernel": "layout.hip", "route_scan_kernel": "layout.hip",
                   "route_finalize_kernel": "layout.hip", "route_single_kernel": "layout.hip",
                   "dispatch_bf16_kernel": "dispatch.hip", "dispatch_fp8_kernel": "dispatch.hip",
-                  "combine_kernel": "combine.hip", "fused_bf16_kernel": "dispatch.hip",
-                  "fused_fp8_kernel": "dispatch.hip"}
+                  "combine_kernel": "combine.hip", "fused_bf16_kernel": "dispatch.hip"}
 
 
 def source_hash(kernel):
@@ -115,6 +118,9 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         rec = {"kernels": {}}
+    # Entries taken on older kernel sources no longer describe any kernel: drop them.
+    rec["kernels"] = {k: v for k, v in rec.get("kernels", {}).items()
+                      if v.get("source_hash") == source_hash(k.split("@")[0])}
     rec["calibration"] = {"fetch_factor": round(fetch_factor, 4), "write_factor": round(write_factor, 4),
                           "copy_bytes_each_way": int(n), "copy_fetch_kib": float(np.median(cf)),
                           "copy_write_kib": float(np.median(cw))}
@@ -137,6 +143,41 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
     txt = os.path.join(ROOT, "profiles", "hbm_counters_%s.txt" % workload)
     open(txt, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def device_info(torch):
+    """The GPU's identity and the settings that move HBM-bound numbers between boxes (memory vendor,
+    current memory clock, package power cap), read from torch and from the amdgpu driver's sysfs
+    files of the same PCI device (no child process); missing fields are null."""
+    import glob
+
+    p = torch.cuda.get_device_properties(0)
+    info = {"arch": p.gcnArchName.split(":")[0], "cus": p.multi_processor_count,
+            "hbm_gib": round(p.total_memory / 2 ** 30, 1), "memory_vendor": None, "mclk_mhz": None,
+            "max_package_power_w": None}
+    bdf = "%04x:%02x:%02x." % (p.pci_domain_id, p.pci_bus_id, p.pci_device_id)
+    for card in glob.glob("/sys/class/drm/card[0-9]*"):
+        dev = os.path.join(card, "device")
+        if "-" in os.path.basename(card) or not os.path.basename(os.path.realpath(dev)).startswith(bdf):
+            continue
+        try:
+            info["memory_vendor"] = open(os.path.join(dev, "mem_info_vram_vendor")).read().strip()
+        except OSError:
+            pass
+        try:
+            for line in open(os.path.join(dev, "pp_dpm_mclk")).read().splitlines():
+                if line.rstrip().endswith("*"):  # the current level
+                    info["mclk_mhz"] = int(line.split(":")[1].strip(" *").lower().replace("mhz", ""))
+        except (OSError, ValueError, IndexError):
+            pass
+        try:
+            cap = sorted(glob.glob(os.path.join(dev, "hwmon", "hwmon*", "power1_cap")))
+            if cap:
+                info["max_package_power_w"] = int(open(cap[0]).read()) / 1e6  # microwatts
+        except (OSError, ValueError):
+            pass
+        break
+    return info
 
 
 def cpu_baseline(w, idx, x, gw, budget_s):
@@ -247,17 +288,23 @@ def main():
         y = recv
 
     def step(i, ev=None):
-        # With --fused the layout leg is empty and the dispatch leg is the fused call.
-        if ev is not None:
-            ev[0].record(stream)
-        if not args.fused:
-            epl.layout(cfg, idx_d, out=L)
-        if ev is not None:
-            ev[1].record(stream)
-        if args.fused:
+        # Without events the default path is one epl_layout_dispatch call; with events it is
+        # issued as its two phases, so the legs are epl_layout_counts and epl_dispatch_rows.
+        if args.fused and ev is None:
             epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
         else:
-            epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
+            if ev is not None:
+                ev[0].record(stream)
+            if args.fused:
+                epl.layout_counts(cfg, idx_d, out=L)
+            else:
+                epl.layout(cfg, idx_d, out=L)
+            if ev is not None:
+                ev[1].record(stream)
+            if args.fused:
+                epl.dispatch_rows(cfg, idx_d, xs[i % n_x], L, recv, recv_scale)
+            else:
+                epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
         if ev is not None:
             ev[2].record(stream)
         epl.combine(cfg, y, w_d, L, out)
@@ -311,14 +358,19 @@ def main():
             graphs[i % n_x].replay()
             continue
         ev = dev_ev.get(i)
-        if not args.fused:
-            epl.layout(cfg, idx_d, out=L)
-        if ev is not None and dom == "dispatch":
-            ev[0].record(stream)
-        if args.fused:
+        if args.fused and not (ev is not None and dom == "dispatch"):
             epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
         else:
-            epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
+            if args.fused:
+                epl.layout_counts(cfg, idx_d, out=L)
+            else:
+                epl.layout(cfg, idx_d, out=L)
+            if ev is not None:
+                ev[0].record(stream)
+            if args.fused:
+                epl.dispatch_rows(cfg, idx_d, xs[i % n_x], L, recv, recv_scale)
+            else:
+                epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
         if ev is not None:
             ev[1 if dom == "dispatch" else 0].record(stream)
         epl.combine(cfg, y, w_d, L, out)
@@ -342,11 +394,9 @@ def main():
         dom_us = float(np.mean(per[:, 1 if dom == "dispatch" else 2]))
 
     pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
-    if args.fused:
-        percentiles = {"layout_dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]), "layer": pct(per.sum(axis=1))}
-    else:
-        percentiles = {"layout": pct(per[:, 0]), "dispatch": pct(per[:, 1]), "combine": pct(per[:, 2]),
-                       "layer": pct(per.sum(axis=1))}
+    legs = ("layout_counts", "dispatch_rows") if args.fused else ("layout", "dispatch")
+    percentiles = {legs[0]: pct(per[:, 0]), legs[1]: pct(per[:, 1]), "combine": pct(per[:, 2]),
+                   "layer": pct(per.sum(axis=1))}
 
     nbytes = algorithmic_bytes(w.T, w.k, w.H, w.R, w.E, P, w.payload)
     value = nbytes["total"] / (ms_per_step * 1e-3) / 1e9
@@ -356,16 +406,18 @@ def main():
     fabric_pairs = int(rc.sum() - np.trace(rc))
     row_bytes = w.H * 2 if w.payload == "bf16" else w.H + (w.H // 128) * 4
 
-    achieved = nbytes[dom] / (dom_us * 1e-6) / 1e9
-    kname = {"dispatch": "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
-             "combine": "combine_kernel"}[dom]
+    # The dispatch leg is one kernel: the plain dispatch kernel, or (epl_dispatch_rows with the
+    # layout's finalize fused in) the fused row kernel, whose bytes include the placement metadata.
     launches = epl.layout_dispatch_launches(cfg) if args.fused else None
-    if args.fused and dom == "dispatch":
-        # The events bracket the whole epl_layout_dispatch call, the layout's other kernels included.
-        kname = "epl_layout_dispatch (%d kernels%s)" % (launches, ", finalize fused" if launches == 3 else "")
+    row_fused = args.fused and launches == 3
+    dom_bytes = nbytes["rows_fused" if row_fused and dom == "dispatch" else dom]
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    kname = {"dispatch": "fused_bf16_kernel" if row_fused else
+             "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
+             "combine": "combine_kernel"}[dom]
     roofline = {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": load_traffic(kname, w.name), "algorithmic_bytes": nbytes[dom],
+                "traffic": load_traffic(kname, w.name), "algorithmic_bytes": dom_bytes,
                 "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev) if dev_ev else args.steps}
 
     cpu = None
@@ -384,11 +436,11 @@ def main():
         "config": {"workload": w.name, "ranks": w.R, "experts": w.E, "topk": w.k, "tokens_per_rank": w.T // w.R,
                    "hidden": w.H, "payload": w.payload, "routing": w.routing, "pairs": P, "seed": args.seed},
         "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_instrumented": round(us_layer_events, 2),
-        "us_layout": None if args.fused else round(us_layout, 2),
-        "us_dispatch": None if args.fused else round(us_dispatch, 2),
-        "us_layout_dispatch": round(us_dispatch + (0.0 if args.fused else us_layout), 2),
+        "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2),
+        "us_layout_dispatch": round(us_dispatch + us_layout, 2),
         "us_combine": round(us_combine, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
+        "device": device_info(torch),
         "launch": "graph" if graphs is not None else "eager",
         "calls": "epl_layout_dispatch + epl_combine" if args.fused else "epl_layout + epl_dispatch + epl_combine",
         "layout_dispatch_launches": launches,

@@ -140,10 +140,27 @@ epl_status epl_dispatch(const epl_config *cfg, const void *x, const epl_layout_b
  * rows, dedup slots) runs inside the dispatch kernel, which saves a launch; other configs run the
  * layout and then the dispatch (see epl_layout_dispatch_launches). Arguments are those of the two
  * calls, with the same meaning, alignment and capacity rules; every status those calls can
- * return is returned before any launch.                                                      */
+ * return is returned before any launch. It is exactly epl_layout_counts followed by
+ * epl_dispatch_rows with the same arguments.                                                 */
 epl_status epl_layout_dispatch(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
                                void *workspace, size_t workspace_bytes, const void *x, void *recv, float *recv_scale,
                                int64_t recv_rows_cap, void *stream);
+
+/* The two phases of epl_layout_dispatch, for callers that put work between them or time them
+ * apart (Kernel Decomposition: counts and prefix sums, then sending and reordering).
+ * epl_layout_counts launches the layout kernels the row kernel does not take over: histogram
+ * and scan when the finalize step is fused into the row kernel, otherwise the whole layout. On
+ * return (stream order) send_cnt, rank_cnt, tok_nranks and num_invalid are final; the other
+ * fields of L are final only after epl_dispatch_rows. Statuses as epl_layout.
+ * epl_dispatch_rows launches exactly one kernel: the fused finalize-and-send kernel, or the
+ * plain dispatch kernel. It must follow epl_layout_counts on the same stream (or be ordered
+ * after it) with the same cfg, topk_idx, L and workspace, none of them changed in between;
+ * otherwise its outputs are undefined. Statuses as epl_layout_dispatch, all before the launch. */
+epl_status epl_layout_counts(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                             void *workspace, size_t workspace_bytes, void *stream);
+epl_status epl_dispatch_rows(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                             void *workspace, size_t workspace_bytes, const void *x, void *recv, float *recv_scale,
+                             int64_t recv_rows_cap, void *stream);
 
 /* Combine: gate-weighted gather-reduce of expert output rows back into token order (the
  * paper's combine: gather expert outputs, restore token order).
@@ -170,7 +187,8 @@ int epl_layout_launches(const epl_config *cfg);
 
 /* Kernel launches epl_layout_dispatch issues for cfg: 2 (one-launch layout, dispatch),
  * 3 (histogram, scan, finalize fused into the dispatch) or 4 (three-launch layout, dispatch).
- * Returns -1 if cfg is invalid. Host-only, no HIP calls.                                      */
+ * epl_layout_counts issues all but the last of them. Returns -1 if cfg is invalid. Host-only,
+ * no HIP calls.                                                                               */
 int epl_layout_dispatch_launches(const epl_config *cfg);
 
 /* Static strings; never NULL. */

@@ -75,8 +75,11 @@ EPL_EXPORT size_t epl_workspace_bytes(const epl_config* cfg) {
   return workspace_bytes(make_geom(cfg));
 }
 
-EPL_EXPORT epl_status epl_layout(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
-                                 void* workspace, size_t ws_bytes, void* stream) {
+namespace {
+
+// The checks of epl_layout (topk_idx, L, workspace), shared by the calls that run the layout.
+epl_status check_layout_args(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                             void* workspace, size_t ws_bytes) {
   epl_status st = check_config(cfg);
   if (st != EPL_OK) return st;
   if ((st = check_layout_buffers(L)) != EPL_OK) return st;
@@ -86,8 +89,58 @@ EPL_EXPORT epl_status epl_layout(const epl_config* cfg, const int32_t* topk_idx,
   if (!workspace) return EPL_ERR_WORKSPACE;
   if (!aligned(workspace, 4)) return EPL_ERR_ALIGN;
   if (ws_bytes < workspace_bytes(g)) return EPL_ERR_WORKSPACE;
-  return from_hip(epl::launch_layout(g, topk_idx, static_cast<int32_t*>(workspace), L->send_cnt, L->rank_cnt,
-                                     L->expert_off, L->rank_off, L->seg_off, L->tok_nranks, L->pair_row,
+  return EPL_OK;
+}
+
+// The layout checks plus those of epl_dispatch (x, recv, recv_scale, capacity).
+epl_status check_layout_dispatch(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                 void* workspace, size_t ws_bytes, const void* x, void* recv, float* recv_scale,
+                                 int64_t recv_rows_cap) {
+  epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  const bool fp8 = cfg->payload == EPL_PAYLOAD_FP8_E4M3;
+  if (fp8 && cfg->hidden % 128 != 0) return EPL_ERR_UNSUPPORTED;
+  if ((st = check_layout_args(cfg, topk_idx, L, workspace, ws_bytes)) != EPL_OK) return st;
+  const epl::Geom g = make_geom(cfg);
+  if (g.T > 0 && (!x || !recv || (fp8 && !recv_scale))) return EPL_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(recv, 16) || (fp8 && !aligned(recv_scale, 4))) return EPL_ERR_ALIGN;
+  if (recv_rows_cap < g.T * cfg->topk) return EPL_ERR_CAPACITY;
+  return EPL_OK;
+}
+
+bool rows_fused(const epl::Geom& g, const epl_config* cfg) {
+  return !epl::layout_single(g) && epl::fused_dispatch_ok(g, cfg->payload == EPL_PAYLOAD_FP8_E4M3);
+}
+
+// The layout kernels the row kernel does not take over: histogram and scan when the finalize
+// step is fused into the row kernel, otherwise the whole layout.
+hipError_t run_counts(const epl::Geom& g, const epl_config* cfg, const int32_t* topk_idx,
+                      const epl_layout_buffers* L, int32_t* ws, hipStream_t s) {
+  if (rows_fused(g, cfg))
+    return epl::launch_layout_counts(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->tok_nranks, L->num_invalid, s);
+  return epl::launch_layout(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->expert_off, L->rank_off, L->seg_off,
+                            L->tok_nranks, L->pair_row, L->pair_rslot, L->recv_src, L->recv_j, L->num_invalid, s);
+}
+
+// One kernel: the fused finalize-and-send kernel, or the plain bf16 / fp8 dispatch kernel.
+hipError_t run_rows(const epl::Geom& g, const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                    int32_t* ws, const void* x, void* recv, float* recv_scale, int64_t cap, hipStream_t s) {
+  if (rows_fused(g, cfg))
+    return epl::launch_fused_dispatch(g, topk_idx, ws, L->expert_off, L->rank_off, L->seg_off, L->pair_row,
+                                      L->pair_rslot, L->recv_src, L->recv_j, x, recv, cfg->hidden, cap, s);
+  if (cfg->payload == EPL_PAYLOAD_FP8_E4M3)
+    return epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden, cap, s);
+  return epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, cap, s);
+}
+
+}  // namespace
+
+EPL_EXPORT epl_status epl_layout(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                 void* workspace, size_t ws_bytes, void* stream) {
+  const epl_status st = check_layout_args(cfg, topk_idx, L, workspace, ws_bytes);
+  if (st != EPL_OK) return st;
+  return from_hip(epl::launch_layout(make_geom(cfg), topk_idx, static_cast<int32_t*>(workspace), L->send_cnt,
+                                     L->rank_cnt, L->expert_off, L->rank_off, L->seg_off, L->tok_nranks, L->pair_row,
                                      L->pair_rslot, L->recv_src, L->recv_j, L->num_invalid,
                                      static_cast<hipStream_t>(stream)));
 }
@@ -110,50 +163,37 @@ EPL_EXPORT epl_status epl_dispatch(const epl_config* cfg, const void* x, const e
   return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, T, cfg->topk, cfg->hidden, recv_rows_cap, s));
 }
 
+
+EPL_EXPORT epl_status epl_layout_counts(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                        void* workspace, size_t ws_bytes, void* stream) {
+  const epl_status st = check_layout_args(cfg, topk_idx, L, workspace, ws_bytes);
+  if (st != EPL_OK) return st;
+  return from_hip(run_counts(make_geom(cfg), cfg, topk_idx, L, static_cast<int32_t*>(workspace),
+                             static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT epl_status epl_dispatch_rows(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                        void* workspace, size_t ws_bytes, const void* x, void* recv,
+                                        float* recv_scale, int64_t recv_rows_cap, void* stream) {
+  const epl_status st =
+      check_layout_dispatch(cfg, topk_idx, L, workspace, ws_bytes, x, recv, recv_scale, recv_rows_cap);
+  if (st != EPL_OK) return st;
+  return from_hip(run_rows(make_geom(cfg), cfg, topk_idx, L, static_cast<int32_t*>(workspace), x, recv, recv_scale,
+                           recv_rows_cap, static_cast<hipStream_t>(stream)));
+}
+
 EPL_EXPORT epl_status epl_layout_dispatch(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
                                           void* workspace, size_t ws_bytes, const void* x, void* recv,
                                           float* recv_scale, int64_t recv_rows_cap, void* stream) {
-  epl_status st = check_config(cfg);
+  const epl_status st =
+      check_layout_dispatch(cfg, topk_idx, L, workspace, ws_bytes, x, recv, recv_scale, recv_rows_cap);
   if (st != EPL_OK) return st;
-  const bool fp8 = cfg->payload == EPL_PAYLOAD_FP8_E4M3;
-  if (fp8 && cfg->hidden % 128 != 0) return EPL_ERR_UNSUPPORTED;
-  if ((st = check_layout_buffers(L)) != EPL_OK) return st;
   const epl::Geom g = make_geom(cfg);
-  if (g.T > 0 && (!topk_idx || !x || !recv || (fp8 && !recv_scale))) return EPL_ERR_INVALID_ARG;
-  if (!aligned(topk_idx, 4) || !aligned(x, 16) || !aligned(recv, 16) || (fp8 && !aligned(recv_scale, 4)))
-    return EPL_ERR_ALIGN;
-  if (recv_rows_cap < g.T * cfg->topk) return EPL_ERR_CAPACITY;
-  if (!workspace) return EPL_ERR_WORKSPACE;
-  if (!aligned(workspace, 4)) return EPL_ERR_ALIGN;
-  if (ws_bytes < workspace_bytes(g)) return EPL_ERR_WORKSPACE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* ws = static_cast<int32_t*>(workspace);
-  if (epl::layout_single(g)) {  // small layouts: the one-launch layout, then the dispatch
-    const hipError_t e = epl::launch_layout(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->expert_off, L->rank_off,
-                                            L->seg_off, L->tok_nranks, L->pair_row, L->pair_rslot, L->recv_src,
-                                            L->recv_j, L->num_invalid, s);
-    if (e != hipSuccess) return EPL_ERR_DEVICE;
-    if (fp8)
-      return from_hip(epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden,
-                                               recv_rows_cap, s));
-    return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, recv_rows_cap, s));
-  }
-  if (!epl::fused_dispatch_ok(g, fp8)) {  // three-launch layout, then the dispatch
-    const hipError_t e = epl::launch_layout(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->expert_off, L->rank_off,
-                                            L->seg_off, L->tok_nranks, L->pair_row, L->pair_rslot, L->recv_src,
-                                            L->recv_j, L->num_invalid, s);
-    if (e != hipSuccess) return EPL_ERR_DEVICE;
-    if (fp8)
-      return from_hip(epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden,
-                                               recv_rows_cap, s));
-    return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, recv_rows_cap, s));
-  }
-  const hipError_t e = epl::launch_layout_counts(g, topk_idx, ws, L->send_cnt, L->rank_cnt, L->tok_nranks,
-                                                 L->num_invalid, s);
-  if (e != hipSuccess) return EPL_ERR_DEVICE;
-  return from_hip(epl::launch_fused_dispatch(g, topk_idx, ws, L->expert_off, L->rank_off, L->seg_off, L->pair_row,
-                                             L->pair_rslot, L->recv_src, L->recv_j, x, recv, cfg->hidden,
-                                             recv_rows_cap, s));
+  const hipError_t e = run_counts(g, cfg, topk_idx, L, ws, s);
+  if (e != hipSuccess) return from_hip(e);
+  return from_hip(run_rows(g, cfg, topk_idx, L, ws, x, recv, recv_scale, recv_rows_cap, s));
 }
 
 EPL_EXPORT int epl_layout_dispatch_launches(const epl_config* cfg) {

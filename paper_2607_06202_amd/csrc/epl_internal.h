@@ -171,6 +171,10 @@ bool layout_single(const Geom& g);  // true if epl_layout runs as one launch for
 // finalize step (route_finalize_kernel, or the fused finalize in the dispatch kernels).
 hipError_t launch_layout_counts(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
                                 int32_t* tok_nranks, int32_t* num_invalid, hipStream_t stream);
+// K3 only, after launch_layout_counts on the same stream.
+hipError_t launch_layout_finalize(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* expert_off,
+                                  int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
+                                  int32_t* recv_src, int32_t* recv_j, hipStream_t stream);
 hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* send_cnt, int32_t* rank_cnt,
                          int32_t* expert_off, int32_t* rank_off, int32_t* seg_off, int32_t* tok_nranks,
                          int32_t* pair_row, int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j,

@@ -659,6 +659,13 @@ hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t
   }
   hipError_t err = launch_layout_counts(g, idx, ws, send_cnt, rank_cnt, tok_nranks, num_invalid, stream);
   if (err != hipSuccess) return err;
+  return launch_layout_finalize(g, idx, ws, expert_off, rank_off, seg_off, pair_row, pair_rslot, recv_src, recv_j,
+                                stream);
+}
+
+hipError_t launch_layout_finalize(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* expert_off,
+                                  int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
+                                  int32_t* recv_src, int32_t* recv_j, hipStream_t stream) {
   const WsLayout wl = ws_layout(g);
   hipLaunchKernelGGL(route_finalize_kernel, dim3(g.nblk), dim3(kLayoutThreads), finalize_lds_bytes(g), stream, g,
                      idx, ws + wl.chunk_e, ws + wl.chunk_r, ws + wl.recv_cnt, ws + wl.seg_rel,

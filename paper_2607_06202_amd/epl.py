@@ -87,6 +87,10 @@ def lib() -> ctypes.CDLL:
         L.epl_version.argtypes = []
         L.epl_layout_dispatch.restype = ctypes.c_int
         L.epl_layout_dispatch.argtypes = [CP, P, LP, P, S, P, P, P, I64, P]
+        L.epl_layout_counts.restype = ctypes.c_int
+        L.epl_layout_counts.argtypes = [CP, P, LP, P, S, P]
+        L.epl_dispatch_rows.restype = ctypes.c_int
+        L.epl_dispatch_rows.argtypes = [CP, P, LP, P, S, P, P, P, I64, P]
         L.epl_layout_dispatch_launches.restype = ctypes.c_int
         L.epl_layout_dispatch_launches.argtypes = [CP]
         L.epl_layout_launches.restype = ctypes.c_int
@@ -178,20 +182,39 @@ def _rows_of(t: torch.Tensor, name: str, width: int) -> int:
     return t.shape[0]
 
 
-def layout(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> Layout:
-    """epl_layout: topk_idx [T, k] int32 on the GPU -> Layout."""
-    dev = topk_idx.device
+def _layout_args(cfg: Config, topk_idx: torch.Tensor, out: Layout | None) -> Layout:
+    """Checks shared by the calls that run the layout; returns the Layout to fill."""
     _dev(topk_idx, "topk_idx", torch.int32)
     if topk_idx.numel() != cfg.T * cfg.topk:
         raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
-    L = out if out is not None else alloc_layout(cfg, dev)
-    _check_layout(cfg, L, dev)
+    L = out if out is not None else alloc_layout(cfg, topk_idx.device)
+    _check_layout(cfg, L, topk_idx.device)
     if L.workspace.numel() < workspace_bytes(cfg):
         raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), workspace_bytes(cfg)))
+    return L
+
+
+def layout(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> Layout:
+    """epl_layout: topk_idx [T, k] int32 on the GPU -> Layout."""
+    dev = topk_idx.device
+    L = _layout_args(cfg, topk_idx, out)
     bufs = L.buffers()
     with _on(dev):
         _check(lib().epl_layout(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs), L.workspace.data_ptr(),
                                 L.workspace.numel(), _stream(dev)), "epl_layout")
+    return L
+
+
+def layout_counts(cfg: Config, topk_idx: torch.Tensor, out: Layout | None = None) -> Layout:
+    """epl_layout_counts: first phase of layout_dispatch (the layout kernels the row kernel does
+    not take over) -> Layout, complete only after dispatch_rows."""
+    dev = topk_idx.device
+    L = _layout_args(cfg, topk_idx, out)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_layout_counts(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                       L.workspace.data_ptr(), L.workspace.numel(), _stream(dev)),
+               "epl_layout_counts")
     return L
 
 
@@ -233,20 +256,12 @@ def dispatch(cfg: Config, x: torch.Tensor, L: Layout, recv: torch.Tensor | None 
     return recv, recv_scale
 
 
-def layout_dispatch(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: Layout | None = None,
-                    recv: torch.Tensor | None = None, recv_scale: torch.Tensor | None = None):
-    """epl_layout_dispatch: layout and dispatch in one call -> (Layout, recv, recv_scale | None)."""
-    dev = topk_idx.device
-    _dev(topk_idx, "topk_idx", torch.int32)
-    if topk_idx.numel() != cfg.T * cfg.topk:
-        raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
+def _recv_args(cfg: Config, x: torch.Tensor, recv, recv_scale, dev):
+    """Checks of x, recv and recv_scale shared by the dispatching calls -> (recv, recv_scale,
+    scale pointer or None, recv rows)."""
     _dev(x, "x", torch.bfloat16)
     if _rows_of(x, "x", cfg.hidden) < cfg.T:
         raise ValueError("x has %d rows, needs T = %d" % (x.shape[0], cfg.T))
-    L = out if out is not None else alloc_layout(cfg, dev)
-    _check_layout(cfg, L, dev)
-    if L.workspace.numel() < workspace_bytes(cfg):
-        raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), workspace_bytes(cfg)))
     if recv is None:
         recv, recv_scale = alloc_recv(cfg, dev)
     fp8 = cfg.payload == PAYLOAD_FP8_E4M3
@@ -258,12 +273,36 @@ def layout_dispatch(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: L
         if _rows_of(recv_scale, "recv_scale", cfg.hidden // 128) < rows:
             raise ValueError("recv_scale has fewer rows than recv")
     _same_device(dev, x=x, recv=recv, recv_scale=recv_scale if fp8 else None)
+    return recv, recv_scale, sp, rows if recv.numel() else 0
+
+
+def layout_dispatch(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: Layout | None = None,
+                    recv: torch.Tensor | None = None, recv_scale: torch.Tensor | None = None):
+    """epl_layout_dispatch: layout and dispatch in one call -> (Layout, recv, recv_scale | None)."""
+    dev = topk_idx.device
+    L = _layout_args(cfg, topk_idx, out)
+    recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
     bufs = L.buffers()
     with _on(dev):
         _check(lib().epl_layout_dispatch(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
                                          L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
-                                         sp, rows if recv.numel() else 0, _stream(dev)), "epl_layout_dispatch")
+                                         sp, rows, _stream(dev)), "epl_layout_dispatch")
     return L, recv, recv_scale
+
+
+def dispatch_rows(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, L: Layout, recv: torch.Tensor | None = None,
+                  recv_scale: torch.Tensor | None = None):
+    """epl_dispatch_rows: second phase of layout_dispatch, one kernel, after layout_counts on the
+    same stream with the same topk_idx and L -> (recv, recv_scale | None)."""
+    dev = topk_idx.device
+    _layout_args(cfg, topk_idx, L)
+    recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_dispatch_rows(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                       L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
+                                       sp, rows, _stream(dev)), "epl_dispatch_rows")
+    return recv, recv_scale
 
 
 def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):
@@ -313,7 +352,8 @@ def layout_launches(cfg: Config) -> int:
 
 
 def layout_dispatch_launches(cfg: Config) -> int:
-    """Kernel launches epl_layout_dispatch issues for cfg: 2, 3 (finalize fused into dispatch) or 4."""
+    """Kernel launches epl_layout_dispatch issues for cfg: 2, 3 (finalize fused into dispatch) or 4;
+    layout_counts issues all but the last."""
     n = lib().epl_layout_dispatch_launches(ctypes.byref(cfg))
     if n < 0:
         raise EplError(1, "epl_layout_dispatch_launches")

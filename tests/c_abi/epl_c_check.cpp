@@ -73,8 +73,13 @@ struct Case {
   epl_payload payload;
 };
 
-// With fused, layout and dispatch run as one epl_layout_dispatch call.
-bool run_case(const Case& c, uint64_t seed, hipStream_t stream, bool fused) {
+// How layout and dispatch are called: epl_layout then epl_dispatch, one epl_layout_dispatch
+// call, or its two phases epl_layout_counts then epl_dispatch_rows.
+enum Mode { kSeparate, kOneCall, kTwoPhases };
+const char* const kModeName[] = {"epl_layout + epl_dispatch", "epl_layout_dispatch",
+                                 "epl_layout_counts + epl_dispatch_rows"};
+
+bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
   const int64_t T = (int64_t)c.R * c.Tr, Tk = T * c.k;
   const bool fp8 = c.payload == EPL_PAYLOAD_FP8_E4M3;
   std::vector<int32_t> idx(Tk);
@@ -122,9 +127,15 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, bool fused) {
   uint16_t* d_o = nullptr;
   HIP_OK(hipMalloc(&d_o, (size_t)std::max<int64_t>(T, 1) * c.H * 2));
 
-  bool ok = fused ? epl_layout_dispatch(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk, stream) == EPL_OK
-                  : (epl_layout(&cfg, d_idx, &L, ws, ws_bytes, stream) == EPL_OK &&
-                     epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk, stream) == EPL_OK);
+  bool ok;
+  if (mode == kOneCall)
+    ok = epl_layout_dispatch(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk, stream) == EPL_OK;
+  else if (mode == kTwoPhases)
+    ok = epl_layout_counts(&cfg, d_idx, &L, ws, ws_bytes, stream) == EPL_OK &&
+         epl_dispatch_rows(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk, stream) == EPL_OK;
+  else
+    ok = epl_layout(&cfg, d_idx, &L, ws, ws_bytes, stream) == EPL_OK &&
+         epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk, stream) == EPL_OK;
   ok = ok && epl_combine(&cfg, d_y, d_w, &L, d_o, stream) == EPL_OK;
   if (!ok) std::printf("a call returned an error status\n");
   HIP_OK(hipStreamSynchronize(stream));
@@ -164,6 +175,12 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, bool fused) {
              EPL_ERR_CAPACITY &&
          epl_layout_dispatch(&cfg, d_idx, &L, ws, ws_bytes - 4, d_x, d_recv, d_scale, Tk, stream) ==
              EPL_ERR_WORKSPACE &&
+         epl_layout_counts(&cfg, d_idx, &L, ws, ws_bytes - 4, stream) == EPL_ERR_WORKSPACE &&
+         epl_layout_counts(&bad, d_idx, &L, ws, ws_bytes, stream) == EPL_ERR_INVALID_ARG &&
+         epl_dispatch_rows(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk - 1, stream) ==
+             EPL_ERR_CAPACITY &&
+         epl_dispatch_rows(&cfg, d_idx, &L, ws, ws_bytes, (char*)d_x + 2, d_recv, d_scale, Tk, stream) ==
+             EPL_ERR_ALIGN &&
          epl_combine(&cfg, d_y, d_w, &L, (char*)d_o + 8, stream) == EPL_ERR_ALIGN;
     if (!ok) std::printf("an invalid call was not rejected with the documented status\n");
   }
@@ -178,8 +195,9 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, bool fused) {
   if (d_scale) HIP_OK(hipFree(d_scale));
   HIP_OK(hipFree(d_o));
   std::printf("case R=%d E=%d k=%d Tr=%d H=%d %s %s (%d launches): %s\n", c.R, c.E, c.k, c.Tr, c.H,
-              fp8 ? "fp8" : "bf16", fused ? "epl_layout_dispatch" : "epl_layout + epl_dispatch",
-              fused ? epl_layout_dispatch_launches(&cfg) : epl_layout_launches(&cfg) + 1, ok ? "ok" : "FAILED");
+              fp8 ? "fp8" : "bf16", kModeName[mode],
+              mode == kSeparate ? epl_layout_launches(&cfg) + 1 : epl_layout_dispatch_launches(&cfg),
+              ok ? "ok" : "FAILED");
   return ok;
 }
 
@@ -193,13 +211,13 @@ int main() {
       {8, 32, 4, 50, 1024, EPL_PAYLOAD_BF16},     // one-launch layout
       {4, 16, 8, 100, 512, EPL_PAYLOAD_FP8_E4M3},  // fp8, one-launch layout
       {32, 256, 8, 80, 256, EPL_PAYLOAD_BF16},    // T*k = 20480: three-launch layout
+      {64, 256, 8, 40, 1024, EPL_PAYLOAD_BF16},   // finalize fused into the row kernel
       {2, 8, 3, 0, 64, EPL_PAYLOAD_BF16},         // no tokens
   };
   bool ok = true;
   uint64_t seed = 12345;
   for (const Case& c : cases) {
-    ok = run_case(c, seed, stream, false) && ok;
-    ok = run_case(c, seed, stream, true) && ok;
+    for (Mode m : {kSeparate, kOneCall, kTwoPhases}) ok = run_case(c, seed, stream, m) && ok;
     ++seed;
   }
   HIP_OK(hipStreamDestroy(stream));

@@ -31,6 +31,17 @@ def test_decode_bytes_from_the_sizes_of_x_and_recv():
     assert abs(b["total"] / (0.7 * 8e12) * 1e6 - 377.9) < 0.05
 
 
+def test_fused_row_kernel_bytes_add_the_placement_metadata():
+    """The row kernel with the layout's finalize step fused in writes the expert, rank and segment
+    offsets, the pair rows and slots, and recv_src / recv_j on top of the dispatch's own bytes."""
+    b = _bytes("decode_ep64")
+    R, E, T, k, P = 64, 256, 8192, 8, 65536
+    placement = 4 * ((E + 1) + (R + 1) + E * R + 2 * T * k + 2 * P)
+    assert placement == 1_115_400
+    assert b["rows_fused"] == b["dispatch"] + placement
+    assert placement < b["layout"]  # the layout still accounts for them once in the total
+
+
 def test_fp8_bytes_include_one_scale_per_128_elements():
     b = _bytes("skewed_fp8_ep64")
     P, H = 16384 * 8, 7168

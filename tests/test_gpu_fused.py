@@ -1,5 +1,6 @@
-"""epl_layout_dispatch against the CPU oracle: every layout output and the bf16 / fp8 payload, bit for
-bit. It takes three paths, and every case asserts which one it exercises:
+"""epl_layout_dispatch, and its two phases epl_layout_counts + epl_dispatch_rows, against the CPU
+oracle: every layout output and the bf16 / fp8 payload, bit for bit. It takes three paths, and every
+case asserts which one it exercises:
 * 3 launches, the layout's finalize step fused into the bf16 dispatch (at most 256 pairs per
   chunk and 256 experts): ragged last chunks, duplicates, invalid ids, 1 and 2 experts per rank,
   more choices than experts;
@@ -17,16 +18,24 @@ from tests.gpu_util import assert_layout_equal, bf16_bits, device, to_dev_bf16
 pytestmark = pytest.mark.gpu
 
 
-def _check(R, E, k, Tr, H, payload, seed, idx=None):
+def _run(cfg, idx_d, x_d, phases):
+    if not phases:
+        return epl.layout_dispatch(cfg, idx_d, x_d)
+    L = epl.layout_counts(cfg, idx_d)
+    recv, sc = epl.dispatch_rows(cfg, idx_d, x_d, L)
+    return L, recv, sc
+
+
+def _check(R, E, k, Tr, H, payload, seed, idx=None, phases=False):
     dev = device()
     T = R * Tr
     if idx is None:
         idx = W.with_replacement(seed, T, k, -1, E + 1).astype(np.int32)
     x = W.normal_bf16(seed, W.STREAM_X, T * H).reshape(T, H)
     cfg = epl.config(R, E, k, H, Tr, payload)
-    L, recv, sc = epl.layout_dispatch(cfg, torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev))
+    L, recv, sc = _run(cfg, torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev), phases)
     torch.cuda.synchronize()
-    what = "R=%d E=%d k=%d Tr=%d H=%d %s" % (R, E, k, Tr, H, payload)
+    what = "R=%d E=%d k=%d Tr=%d H=%d %s%s" % (R, E, k, Tr, H, payload, " (two phases)" if phases else "")
     ref = oracle.layout(R, E, k, Tr, idx)
     assert_layout_equal(L, ref, what)
     if payload == "bf16":
@@ -49,32 +58,37 @@ def _check(R, E, k, Tr, H, payload, seed, idx=None):
     (16, 64, 8, 1024, 64, 6, 4),     # 512 pairs per chunk
     (8, 1024, 32, 1024, 64, 7, 4),   # k = 32, E = 1024
 ])
-def test_layout_dispatch_bf16(R, E, k, Tr, H, seed, launches):
-    cfg, _, _ = _check(R, E, k, Tr, H, "bf16", seed)
+@pytest.mark.parametrize("phases", [False, True])
+def test_layout_dispatch_bf16(R, E, k, Tr, H, seed, launches, phases):
+    cfg, _, _ = _check(R, E, k, Tr, H, "bf16", seed, phases=phases)
     assert epl.layout_dispatch_launches(cfg) == launches
 
 
 @pytest.mark.parametrize("R,E,k,Tr,H,seed", [(64, 256, 8, 40, 1024, 10), (16, 160, 8, 257, 1152, 11)])
-def test_layout_dispatch_fp8(R, E, k, Tr, H, seed):
-    cfg, _, _ = _check(R, E, k, Tr, H, "fp8", seed)
+@pytest.mark.parametrize("phases", [False, True])
+def test_layout_dispatch_fp8(R, E, k, Tr, H, seed, phases):
+    cfg, _, _ = _check(R, E, k, Tr, H, "fp8", seed, phases=phases)
     assert epl.layout_dispatch_launches(cfg) == 4
 
 
-def test_layout_dispatch_small_layout():
-    cfg, _, _ = _check(4, 16, 2, 128, 256, "bf16", 20)
+@pytest.mark.parametrize("phases", [False, True])
+def test_layout_dispatch_small_layout(phases):
+    cfg, _, _ = _check(4, 16, 2, 128, 256, "bf16", 20, phases=phases)
     assert epl.layout_dispatch_launches(cfg) == 2
 
 
-def test_layout_dispatch_all_invalid_and_empty():
-    cfg, _, _ = _check(64, 256, 8, 40, 128, "bf16", 30, idx=np.full((64 * 40, 8), -1, np.int32))
+@pytest.mark.parametrize("phases", [False, True])
+def test_layout_dispatch_all_invalid_and_empty(phases):
+    cfg, _, _ = _check(64, 256, 8, 40, 128, "bf16", 30, idx=np.full((64 * 40, 8), -1, np.int32), phases=phases)
     assert epl.layout_dispatch_launches(cfg) == 3
-    _check(64, 256, 8, 0, 128, "bf16", 31, idx=np.zeros((0, 8), np.int32))
+    _check(64, 256, 8, 0, 128, "bf16", 31, idx=np.zeros((0, 8), np.int32), phases=phases)
 
 
 @pytest.mark.parametrize("name", ["decode_ep64", "skewed_fp8_ep64", "large_ep256", "prefill_ep32"])
 def test_layout_dispatch_matches_separate_calls_at_full_size(name):
-    """The named workloads in the benchmark's configuration: the fused call and epl_layout then
-    epl_dispatch give identical layouts and identical payloads (compared on the device)."""
+    """The named workloads in the benchmark's configuration: the fused call, its two phases and
+    epl_layout then epl_dispatch give identical layouts and identical payloads (compared on the
+    device)."""
     dev = device()
     w = W.WORKLOADS[name]
     idx_d = torch.from_numpy(W.routing(w)).to(dev)
@@ -87,13 +101,16 @@ def test_layout_dispatch_matches_separate_calls_at_full_size(name):
     r1p = r1[:P].clone()
     s1p = None if s1 is None else s1[:P].clone()
     del r1, s1
-    L2, r2, s2 = epl.layout_dispatch(cfg, idx_d, x_d)
-    torch.cuda.synchronize()
-    for n, _ in epl.LayoutBuffers._fields_:
-        a, b = getattr(L1, n), getattr(L2, n)
-        if n in ("recv_src", "recv_j"):
-            a, b = a[:P], b[:P]
-        assert torch.equal(a, b), "%s: %s differs" % (name, n)
-    assert torch.equal(r1p.view(torch.uint8), r2[:P].view(torch.uint8)), name
-    if s1p is not None:
-        assert torch.equal(s1p.view(torch.int32), s2[:P].view(torch.int32)), name
+    for phases in (False, True):
+        L2, r2, s2 = _run(cfg, idx_d, x_d, phases)
+        torch.cuda.synchronize()
+        what = "%s%s" % (name, " (two phases)" if phases else "")
+        for n, _ in epl.LayoutBuffers._fields_:
+            a, b = getattr(L1, n), getattr(L2, n)
+            if n in ("recv_src", "recv_j"):
+                a, b = a[:P], b[:P]
+            assert torch.equal(a, b), "%s: %s differs" % (what, n)
+        assert torch.equal(r1p.view(torch.uint8), r2[:P].view(torch.uint8)), what
+        if s1p is not None:
+            assert torch.equal(s1p.view(torch.int32), s2[:P].view(torch.int32)), what
+        del L2, r2, s2
