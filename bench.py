@@ -203,6 +203,54 @@ def cpu_baseline(w, idx, x, gw, budget_s):
     return el / reps, reps, L.P
 
 
+def calibrate_replicate(torch, epl, w, dev, stream, steps):
+    """The dispatch's byte pattern, one read and k writes per token row, with the k writes
+    contiguous: x [T,H] -> [T,k,H]. Timed two ways on an x of the workload's shape (rotated
+    copies, as in the layer):
+    * torch's broadcast copy (a vendor elementwise kernel);
+    * epl_dispatch itself, on a layout that sends every pair of every token to one expert of one
+      rank, so pair (g, j) lands in row g*k + j (sequential rows instead of the routed scatter)."""
+    x = torch.empty(w.T, w.H, dtype=torch.bfloat16, device=dev).normal_()
+    n_x = max(2, -(-X_ROTATION_BYTES // (x.numel() * 2)))
+    xs = [x] + [x.clone() for _ in range(n_x - 1)]
+    dst = torch.empty(w.T, w.k, w.H, dtype=torch.bfloat16, device=dev)
+    cfg = epl.config(1, 1, w.k, w.H, w.T, "bf16")
+    L = epl.layout(cfg, torch.zeros(w.T, w.k, dtype=torch.int32, device=dev))
+    recv = dst.view(w.T * w.k, w.H)
+    runs = {"torch_broadcast_copy": lambda i: dst.copy_(xs[i % n_x].unsqueeze(1).expand(w.T, w.k, w.H)),
+            "epl_dispatch_sequential_rows": lambda i: epl.dispatch(cfg, xs[i % n_x], L, recv)}
+    nbytes = x.numel() * 2 + dst.numel() * 2
+    out = {"calibration": "replicate x[T,H] -> [T,k,H]", "workload": w.name, "T": w.T, "k": w.k, "H": w.H,
+           "bytes_read": x.numel() * 2, "bytes_written": dst.numel() * 2, "x_copies": n_x}
+    for name, fn in runs.items():
+        for i in range(5):
+            fn(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(steps):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / steps
+        out[name] = {"us": round(us, 2), "GBps": round(nbytes / us / 1e3, 1),
+                     "pct_of_peak": round(100 * nbytes / us / 1e3 / HBM_PEAK_GBS, 2)}
+    ref = torch.empty_like(dst).copy_(xs[(steps - 1) % n_x].unsqueeze(1).expand(w.T, w.k, w.H))
+    epl.dispatch(cfg, xs[(steps - 1) % n_x], L, recv)
+    out["rows_equal"] = bool(torch.equal(ref.view(torch.int16), dst.view(torch.int16)))
+    print(json.dumps(out))
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -216,7 +264,12 @@ def main():
                          "epl_layout_dispatch + epl_combine")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP graph replays of the layer (one graph per x copy) instead of eager launches")
+    ap.add_argument("--warm", action="store_true",
+                    help="read the same x every step (it may stay in the memory-side cache) instead of rotating copies")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
+    ap.add_argument("--calibrate-replicate", action="store_true",
+                    help="time the dispatch's 1-read : k-write byte pattern with sequential rows instead "
+                         "(torch's broadcast copy, and epl_dispatch on an all-to-one layout)")
     ap.add_argument("--ingest-counters", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from rocprofv3 --pmc runs (no GPU needed)")
     ap.add_argument("--command", action="append", default=[], help="profiler command recorded with --ingest-counters")
@@ -263,6 +316,9 @@ def main():
         return
 
     w = W.WORKLOADS[args.workload]
+    if args.calibrate_replicate:
+        calibrate_replicate(torch, epl, w, dev, stream, args.steps)
+        return
     idx = W.routing(w, args.seed)
     x = W.tokens_bf16(w, args.seed)
     gw = W.gate_weights(w, args.seed)
@@ -274,7 +330,7 @@ def main():
     # 256 MB memory-side cache (MALL) in total: every step's dispatch then reads its input from
     # HBM instead of finding the previous step's x still cached.
     x_bytes = x_d.numel() * x_d.element_size()
-    n_x = max(2, -(-X_ROTATION_BYTES // x_bytes)) if x_bytes else 1
+    n_x = max(2, -(-X_ROTATION_BYTES // x_bytes)) if x_bytes and not args.warm else 1
     xs = [x_d] + [x_d.clone() for _ in range(n_x - 1)]
     w_d = torch.from_numpy(gw).to(dev)
     L = epl.alloc_layout(cfg, dev)
@@ -425,6 +481,7 @@ def main():
         sec, reps, P_ref = cpu_baseline(w, idx, x, gw, args.cpu_budget)
         assert P_ref == P
         cpu = {"value": round(nbytes["total"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "cpu_model": cpu_model(),
                "us_per_layer": round(sec * 1e6, 1),
                "sample": "%d full %s layer(s) (layout+dispatch+combine) on the same inputs, single thread" % (
                    reps, w.name)}
@@ -446,7 +503,8 @@ def main():
         "layout_dispatch_launches": launches,
         "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
         "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,
-        "roofline": roofline, "x_copies": n_x, "cpu_baseline": cpu,
+        "roofline": roofline, "x_copies": n_x, "x_reuse": "warm" if args.warm else "rotated",
+        "cpu_baseline": cpu,
     }
     print(json.dumps(rec))
 

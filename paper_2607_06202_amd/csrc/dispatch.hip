@@ -51,10 +51,12 @@ __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int
 // The launcher takes buffer loads for an x of 200 MB or more, a threshold between decode's 117 MB
 // and the 235 MB and 1.9 GB of the others; why the instruction form matters is not established.
 // row_of() returns, in lane j < k, the packed row of pair j (-1 if invalid); it is called after the
-// loads of x are issued, so whatever it loads is in flight together with them.
+// loads of x are issued, so whatever it loads is in flight together with them. An inactive wave
+// loads and calls row_of() (which may hold a workgroup barrier) but stores nothing.
 template <bool BUF_X, class RowFn>
 __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
-                                                   int64_t g, int c, int k, int nv, int64_t cap, int lane) {
+                                                   int64_t g, int c, int k, int nv, int64_t cap, int lane,
+                                                   bool active = true) {
   const u32x4* xr = x + g * nv;
   const int v0 = c * kBf16Cols + lane;
   // Loads are unconditional (index clamped into the row) so that all of them are in flight
@@ -70,6 +72,7 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
     for (int u = 0; u < kBf16VPL; ++u) buf[u] = xr[min(v0 + u * kWave, nv - 1)];
   }
   const int my_row = row_of();
+  if (!active) return;
 #pragma unroll
   for (int u = 0; u < kBf16VPL; ++u) {
     const int v = v0 + u * kWave;
@@ -205,9 +208,12 @@ hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* rec
 // * slot of a first pair = slots of its rank before the chunk (K2) + earlier first pairs of the
 //   chunk bound for that rank; other valid pairs share the slot of their token's first pair on
 //   the same rank.
-// The wave of column chunk 0 also writes the token's pair_row, pair_rslot, recv_src and recv_j.
-// A few extra workgroups at the end of the grid write expert_off, rank_off and seg_off. The loads
-// of x are issued before the row computation, so they are in flight while it runs.
+// A workgroup's waves cover consecutive units, so they share few tokens (one when a row has as
+// many column chunks as the workgroup has waves). Wave w computes the rows of the workgroup's
+// w-th token, writes that token's pair_row, pair_rslot, recv_src and recv_j, and leaves the rows
+// in LDS for the other waves. A few extra workgroups at the end of the grid write expert_off,
+// rank_off and seg_off. The loads of x are issued before the row computation, so they are in
+// flight while it runs.
 struct FusedLayout {
   Geom G;
   const int32_t* idx;
@@ -365,14 +371,33 @@ __global__ void __launch_bounds__(kDispatchThreads)
   }
   const int lane = threadIdx.x % kWave;
   const int w = threadIdx.x / kWave;
-  int32_t* hist = lds + w * (F.G.E + F.G.R);
+  const int k = F.G.k;
+  int32_t* rows_lds = lds;  // [kWavesPerBlock][k]
+  int32_t* hist = lds + kWavesPerBlock * EPL_MAX_TOPK + w * (F.G.E + F.G.R);
   const int64_t units = F.G.T * chunks;
   const int64_t stride = (int64_t)unit_grid * kWavesPerBlock;
-  for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + w; u < units; u += stride) {
-    const int64_t g = u / chunks;
-    const int c = (int)(u - g * chunks);
-    dispatch_bf16_unit<BUF_X>(x, [&] { return token_rows(F, g, c == 0, hist, lane); }, recv, g, c, F.G.k, nv, cap,
-                              lane);
+  // The loop bound depends on the workgroup's first unit only, so every wave runs the same
+  // iterations and reaches the same barriers.
+  for (int64_t ub = (int64_t)blockIdx.x * kWavesPerBlock; ub < units; ub += stride) {
+    const int64_t g_first = ub / chunks;
+    const int64_t g_last = std::min(units - 1, ub + kWavesPerBlock - 1) / chunks;
+    const int64_t u = ub + w;
+    const bool active = u < units;
+    const int64_t g = (active ? u : units - 1) / chunks;
+    const int c = (int)((active ? u : units - 1) - g * chunks);
+    dispatch_bf16_unit<BUF_X>(
+        x,
+        [&] {
+          if (w <= g_last - g_first) {
+            const int r = token_rows(F, g_first + w, true, hist, lane);
+            if (lane < k) rows_lds[w * k + lane] = r;
+          }
+          __syncthreads();
+          const int r = lane < k ? rows_lds[(g - g_first) * k + lane] : -1;
+          __syncthreads();  // every wave has its rows before the next iteration rewrites them
+          return r;
+        },
+        recv, g, c, k, nv, cap, lane, active);
   }
 }
 
@@ -394,7 +419,8 @@ hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws,
   const int64_t units = g.T * chunks;
   const int unit_grid = (int)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30);
   const dim3 grid((unsigned)(unit_grid + nmeta));
-  const size_t lds = sizeof(int32_t) * std::max<size_t>((size_t)kWavesPerBlock * (g.E + g.R), (size_t)g.E + 1);
+  const size_t lds = sizeof(int32_t) * std::max<size_t>((size_t)kWavesPerBlock * (EPL_MAX_TOPK + g.E + g.R),
+                                                        (size_t)g.E + 1);
   const bool buf_x = g.T * (int64_t)H * 2 >= kBufferLoadXBytes;
   const u32x4* xv = static_cast<const u32x4*>(x);
   u32x4* rv = static_cast<u32x4*>(recv);

@@ -99,6 +99,27 @@ def test_layout_both_launch_paths(R, E, k, Tr, launches, vec_ids):
     assert_layout_equal(L, oracle.layout(R, E, k, Tr, idx), "R=%d E=%d k=%d Tr=%d" % (R, E, k, Tr))
 
 
+@pytest.mark.parametrize("R,Tr", [(1, 16384), (2, 8192)])
+def test_every_pair_to_one_expert_per_rank(R, Tr):
+    """k copies of one expert per token, on one expert per rank (E = R), the layout the replicate
+    calibration uses: pair (g, j) of rank s lands in row s*Tr*k + (g - s*Tr)*k + j, i.e. each
+    token's k rows are contiguous and the rows are sequential, for every rank's own tokens. The
+    layout equals the oracle's and that closed form; the payload is x repeated k times."""
+    dev = device()
+    k, H = 8, 64
+    T = R * Tr
+    idx = np.repeat(np.arange(T) // Tr, k).reshape(T, k).astype(np.int32)  # token of rank s -> expert s
+    w = W.Workload("one", R, R, k, Tr, H, "bf16", "-")
+    cfg, L = run_layout(w, idx, dev)
+    x = W.normal_bf16(7, W.STREAM_X, T * H).reshape(T, H)
+    recv, _ = epl.dispatch(cfg, to_dev_bf16(x, dev), L)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, R, k, Tr, idx)
+    assert_layout_equal(L, ref, "one expert per rank, R=%d" % R)
+    np.testing.assert_array_equal(ref.pair_row.reshape(-1), np.arange(T * k))
+    np.testing.assert_array_equal(bf16_bits(recv[:T * k]), np.repeat(x, k, axis=0))
+
+
 def test_layout_empty_and_all_invalid():
     dev = device()
     w = W.Workload("empty", 4, 8, 3, 0, 64, "bf16", "-")
