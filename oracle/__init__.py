@@ -50,6 +50,7 @@ def lib() -> ctypes.CDLL:
             "eplref_quantize_row_e4m3": (None, [I, P, P, P]),
             "eplref_combine": (None, [L, I, I, P, P, P, P, L, P]),
             "eplref_combine_mapped": (None, [I, I, P, P, P, P, P, L, P]),
+            "eplref_locate_rows": (None, [I, P, L, P, P, P]),
             "eplref_f32_to_bf16_array": (None, [P, P, L]),
             "eplref_f32_to_e4m3_array": (None, [P, P, L]),
             "eplref_f32_to_bf16": (ctypes.c_uint16, [ctypes.c_float]),
@@ -174,6 +175,20 @@ def combine_mapped(ys: np.ndarray, row_map: np.ndarray, w: np.ndarray, pair_row:
                                 _p(np.ascontiguousarray(pair_row, dtype=np.int32)), _p(tok), tok.shape[0],
                                 _p(out))
     return out
+
+
+def locate_rows(expert_off: np.ndarray, rows=None, n: int | None = None):
+    """Expert and in-expert offset of packed rows (Token-level Load Partition; Algorithm 1's
+    result): rows, or 0..n-1 when rows is None. Positions outside [0, P) give (-1, -1)."""
+    off = np.ascontiguousarray(expert_off, np.int32)
+    E = off.size - 1
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, np.int32)
+        n = rows.size
+    expert = np.empty(n, np.int32)
+    offset = np.empty(n, np.int32)
+    lib().eplref_locate_rows(E, _p(off), n, None if rows is None else _p(rows), _p(expert), _p(offset))
+    return expert, offset
 
 
 def f32_to_bf16(v: np.ndarray) -> np.ndarray:

@@ -318,3 +318,28 @@ REF_API void eplref_combine_mapped(int k, int H, const uint16_t *ys, const int32
     }
   }
 }
+
+/* ------------------------------------------------------------------------------------------
+ * Row location (Hierarchical Token-level Scheduling, Token-level Load Partition; Algorithm 1):
+ * a global position in the expert-major packed rows is mapped to the expert whose cumulative
+ * range covers it and the position's offset inside that expert's rows. The plain definition
+ * is written out as a linear scan: expert e with expert_off[e] <= r < expert_off[e+1] (the
+ * unique non-empty such e), offset r - expert_off[e]. rows == NULL means r = i for i = 0..n-1.
+ * Positions outside [0, expert_off[E]) get expert -1 and offset -1.
+ * ------------------------------------------------------------------------------------------ */
+REF_API void eplref_locate_rows(int E, const int32_t *expert_off, int64_t n, const int32_t *rows, int32_t *expert,
+                                int32_t *offset) {
+  const int64_t P = expert_off[E];
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t r = rows ? rows[i] : i;
+    expert[i] = -1;
+    offset[i] = -1;
+    if (r < 0 || r >= P) continue;
+    for (int e = 0; e < E; ++e)
+      if (expert_off[e] <= r && r < expert_off[e + 1]) {
+        expert[i] = e;
+        offset[i] = (int32_t)(r - expert_off[e]);
+        break;
+      }
+  }
+}
