@@ -174,6 +174,22 @@ epl_status epl_dispatch_rows(const epl_config *cfg, const int32_t *topk_idx, con
 epl_status epl_combine(const epl_config *cfg, const void *y, const float *topk_w, const epl_layout_buffers *L,
                        void *out, void *stream);
 
+/* Row location (Hierarchical Token-level Scheduling, Token-level Load Partition; Algorithm 1,
+ * Quaternary Search): for each position r, the expert whose cumulative range in the packed rows
+ * covers r and r's offset inside that expert's rows. For a consumer that cuts the P packed rows
+ * into slices (a worker or GEMM tile per slice) and needs the expert at each slice start.
+ *   expert_off [E+1] int32, the layout's expert_off (from epl_layout or epl_layout_dispatch on the
+ *              same stream, or ordered before it); other contents give unspecified but in-bounds
+ *              results.
+ *   rows       [n] int32 positions, or NULL for the positions 0..n-1.
+ *   expert, offset  [n] int32 outputs: expert[i] = e with expert_off[e] <= r < expert_off[e+1]
+ *              (the unique non-empty such e), offset[i] = r - expert_off[e]; both -1 when r is
+ *              outside [0, P), P = expert_off[E].
+ * n >= 0 (INVALID_ARG otherwise); all pointers 4-byte aligned (ALIGN). Only cfg->num_experts is
+ * used beyond the config check.                                                              */
+epl_status epl_locate_rows(const epl_config *cfg, const int32_t *expert_off, const int32_t *rows, int64_t n,
+                           int32_t *expert, int32_t *offset, void *stream);
+
 /* Diagnostics: apply the exact device number conversions used by epl_dispatch (fp32 ->
  * saturating E4M3) and epl_combine (fp32 -> bf16 RNE) to n values, for exhaustive checks.
  * in [n] fp32, out [n] bytes / bf16 bit patterns, 4-byte aligned; n >= 0.                   */

@@ -203,6 +203,17 @@ EPL_EXPORT int epl_layout_dispatch_launches(const epl_config* cfg) {
   return epl::fused_dispatch_ok(g, cfg->payload == EPL_PAYLOAD_FP8_E4M3) ? 3 : 4;
 }
 
+EPL_EXPORT epl_status epl_locate_rows(const epl_config* cfg, const int32_t* expert_off, const int32_t* rows,
+                                      int64_t n, int32_t* expert, int32_t* offset, void* stream) {
+  const epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  if (n < 0) return EPL_ERR_INVALID_ARG;
+  if (n > 0 && (!expert_off || !expert || !offset)) return EPL_ERR_INVALID_ARG;
+  if (!aligned(expert_off, 4) || !aligned(rows, 4) || !aligned(expert, 4) || !aligned(offset, 4)) return EPL_ERR_ALIGN;
+  return from_hip(epl::launch_locate_rows(expert_off, rows, n, cfg->num_experts, expert, offset,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 EPL_EXPORT epl_status epl_combine(const epl_config* cfg, const void* y, const float* topk_w,
                                   const epl_layout_buffers* L, void* out, void* stream) {
   epl_status st = check_config(cfg);

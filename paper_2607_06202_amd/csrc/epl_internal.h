@@ -194,6 +194,8 @@ hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws,
 hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
                           int H, hipStream_t stream);
 
+hipError_t launch_locate_rows(const int32_t* expert_off, const int32_t* rows, int64_t n, int E, int32_t* expert,
+                              int32_t* offset, hipStream_t stream);
 hipError_t launch_debug_e4m3(const float* in, uint8_t* out, int64_t n, hipStream_t stream);
 hipError_t launch_debug_bf16(const float* in, uint16_t* out, int64_t n, hipStream_t stream);
 

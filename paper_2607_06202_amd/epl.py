@@ -91,6 +91,8 @@ def lib() -> ctypes.CDLL:
         L.epl_layout_counts.argtypes = [CP, P, LP, P, S, P]
         L.epl_dispatch_rows.restype = ctypes.c_int
         L.epl_dispatch_rows.argtypes = [CP, P, LP, P, S, P, P, P, I64, P]
+        L.epl_locate_rows.restype = ctypes.c_int
+        L.epl_locate_rows.argtypes = [CP, P, P, I64, P, P, P]
         L.epl_layout_dispatch_launches.restype = ctypes.c_int
         L.epl_layout_dispatch_launches.argtypes = [CP]
         L.epl_layout_launches.restype = ctypes.c_int
@@ -303,6 +305,27 @@ def dispatch_rows(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, L: Layou
                                        L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
                                        sp, rows, _stream(dev)), "epl_dispatch_rows")
     return recv, recv_scale
+
+
+def locate_rows(cfg: Config, L: Layout, rows: torch.Tensor | None = None, n: int | None = None):
+    """epl_locate_rows: expert and in-expert offset of packed rows (rows [n] int32 on the GPU, or
+    the positions 0..n-1 when rows is None) -> (expert [n] int32, offset [n] int32)."""
+    dev = L.expert_off.device
+    if rows is not None:
+        _dev(rows, "rows", torch.int32)
+        _same_device(dev, rows=rows)
+        n = rows.numel()
+    elif n is None or n < 0:
+        raise ValueError("give rows, or n >= 0 for the positions 0..n-1")
+    if L.cfg.num_experts != cfg.num_experts:
+        raise ValueError("layout was allocated for %r, not %r" % (L.cfg, cfg))
+    expert = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    offset = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    with _on(dev):
+        _check(lib().epl_locate_rows(ctypes.byref(cfg), L.expert_off.data_ptr(),
+                                     None if rows is None else rows.data_ptr(), n, expert.data_ptr(),
+                                     offset.data_ptr(), _stream(dev)), "epl_locate_rows")
+    return expert[:n], offset[:n]
 
 
 def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):

@@ -1,7 +1,7 @@
 // Standalone C++ consumer of the C ABI in include/epl.h: no Python, no torch. It allocates
-// device buffers with the HIP runtime, runs layout -> dispatch -> combine on its own stream,
-// and compares every output with the CPU oracle (oracle/liboracle.so, test infrastructure),
-// then checks that host-detectable errors are reported before anything is launched.
+// device buffers with the HIP runtime, runs layout -> dispatch -> combine and the row location on
+// its own stream, and compares every output with the CPU oracle (oracle/liboracle.so, test
+// infrastructure), then checks that host-detectable errors are reported before anything is launched.
 // Prints "c abi check ok" and exits 0 on success; prints the first difference and exits 1.
 #include <hip/hip_runtime_api.h>
 
@@ -23,6 +23,8 @@ void eplref_dispatch_fp8(int64_t T, int k, int H, const uint16_t* x, const int32
                          float* recv_scale);
 void eplref_combine(int64_t T, int k, int H, const uint16_t* y, const float* w, const int32_t* pair_row,
                     const int64_t* tokens, int64_t n_tokens, uint16_t* out);
+void eplref_locate_rows(int E, const int32_t* expert_off, int64_t n, const int32_t* rows, int32_t* expert,
+                        int32_t* offset);
 }
 
 #define HIP_OK(x)                                                                              \
@@ -161,6 +163,19 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
     std::vector<uint16_t> o((size_t)T * c.H);
     eplref_combine(T, c.k, c.H, y.data(), w.data(), r_row.data(), nullptr, T, o.data());
     ok = same("combine", host_copy(d_o, (size_t)T * c.H), o, (size_t)T * c.H);
+  }
+  if (ok) {  // expert and offset of every packed row, and of one position past the end
+    const int64_t n = Tk + 1;
+    std::vector<int32_t> le(n), lo(n);
+    eplref_locate_rows(c.E, r_eoff.data(), n, nullptr, le.data(), lo.data());
+    int32_t *d_le = nullptr, *d_lo = nullptr;
+    HIP_OK(hipMalloc(&d_le, n * 4));
+    HIP_OK(hipMalloc(&d_lo, n * 4));
+    ok = epl_locate_rows(&cfg, d_out[2], nullptr, n, d_le, d_lo, stream) == EPL_OK;
+    HIP_OK(hipStreamSynchronize(stream));
+    ok = ok && same("locate expert", host_copy(d_le, n), le, n) && same("locate offset", host_copy(d_lo, n), lo, n);
+    HIP_OK(hipFree(d_le));
+    HIP_OK(hipFree(d_lo));
   }
 
   // Host-detectable errors come back before any launch.

@@ -1,0 +1,82 @@
+"""epl_locate_rows (Token-level Load Partition; Algorithm 1) against the CPU oracle, position by
+position: every packed row of the named workloads' layouts plus positions past P, random
+positions (negative, duplicated, out of range), 1024 experts that are mostly empty, and empty
+queries. Every row's expert is also checked against the routing table through recv_src/recv_j."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_06202_amd import epl
+from paper_2607_06202_amd import workloads as W
+from tests.gpu_util import device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("name", W.WORKLOAD_ORDER)
+def test_every_row_of_the_named_workloads(name):
+    dev = device()
+    w = W.WORKLOADS[name]
+    idx = W.routing(w)
+    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)
+    L = epl.layout(cfg, torch.from_numpy(idx).to(dev))
+    n = w.T * w.k + 3
+    e, o = epl.locate_rows(cfg, L, n=n)
+    torch.cuda.synchronize()
+    off = L.expert_off.cpu().numpy()
+    want_e, want_o = oracle.locate_rows(off, n=n)
+    np.testing.assert_array_equal(e.cpu().numpy(), want_e, err_msg=name)
+    np.testing.assert_array_equal(o.cpu().numpy(), want_o, err_msg=name)
+    P = int(off[-1])
+    src, j = L.recv_src[:P].cpu().numpy(), L.recv_j[:P].cpu().numpy()
+    np.testing.assert_array_equal(want_e[:P], idx.reshape(-1, w.k)[src, j], err_msg=name)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_positions(seed):
+    dev = device()
+    rng = np.random.default_rng(70 + seed)
+    R, El, k, Tr = [(4, 4, 2, 300), (16, 16, 8, 64), (1, 1, 3, 50), (64, 4, 8, 40)][seed]
+    E, T = R * El, R * Tr
+    idx = W.with_replacement(seed, T, k, -1, E + 1).astype(np.int32)
+    cfg = epl.config(R, E, k, 64, Tr, "bf16")
+    L = epl.layout(cfg, torch.from_numpy(idx).to(dev))
+    rows = rng.integers(-5, T * k + 5, 10_000).astype(np.int32)
+    e, o = epl.locate_rows(cfg, L, torch.from_numpy(rows).to(dev))
+    torch.cuda.synchronize()
+    want_e, want_o = oracle.locate_rows(L.expert_off.cpu().numpy(), rows)
+    np.testing.assert_array_equal(e.cpu().numpy(), want_e)
+    np.testing.assert_array_equal(o.cpu().numpy(), want_o)
+
+
+def test_many_empty_experts_and_empty_queries():
+    dev = device()
+    R, E, k, Tr = 8, 1024, 2, 16  # 256 pairs over 1024 experts: most are empty
+    idx = W.with_replacement(5, R * Tr, k, 0, E).astype(np.int32)
+    cfg = epl.config(R, E, k, 64, Tr, "bf16")
+    L = epl.layout(cfg, torch.from_numpy(idx).to(dev))
+    e, o = epl.locate_rows(cfg, L, n=R * Tr * k)
+    e0, o0 = epl.locate_rows(cfg, L, n=0)
+    e1, o1 = epl.locate_rows(cfg, L, torch.empty(0, dtype=torch.int32, device=dev))
+    torch.cuda.synchronize()
+    want_e, want_o = oracle.locate_rows(L.expert_off.cpu().numpy(), n=R * Tr * k)
+    np.testing.assert_array_equal(e.cpu().numpy(), want_e)
+    np.testing.assert_array_equal(o.cpu().numpy(), want_o)
+    assert e0.numel() == o0.numel() == e1.numel() == o1.numel() == 0
+
+
+def test_rejected_arguments():
+    dev = device()
+    cfg = epl.config(4, 16, 2, 64, 8, "bf16")
+    L = epl.alloc_layout(cfg, dev)
+    out = torch.empty(8, dtype=torch.int32, device=dev)
+    lib, P = epl.lib(), L.expert_off.data_ptr()
+    import ctypes
+    s = epl._stream(dev)
+    assert lib.epl_locate_rows(ctypes.byref(cfg), P, None, -1, out.data_ptr(), out.data_ptr(), s) == 1
+    assert lib.epl_locate_rows(ctypes.byref(cfg), None, None, 4, out.data_ptr(), out.data_ptr(), s) == 1
+    assert lib.epl_locate_rows(ctypes.byref(cfg), P, None, 4, out.data_ptr() + 2, out.data_ptr(), s) == 2
+    bad = epl.config(4, 17, 2, 64, 8, "bf16")
+    assert lib.epl_locate_rows(ctypes.byref(bad), P, None, 4, out.data_ptr(), out.data_ptr(), s) == 1
+    assert lib.epl_locate_rows(ctypes.byref(cfg), None, None, 0, None, None, s) == 0
