@@ -37,7 +37,6 @@ METRIC = "dispatch+combine µs/MoE layer and effective HBM GB/s (% of peak), EP=
 HBM_PEAK_GBS = 8000.0
 X_ROTATION_BYTES = 512 << 20  # twice the MI355X memory-side cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-CSRC = os.path.join(ROOT, "paper_2607_06202_amd", "csrc")
 
 
 def algorithmic_bytes(T, k, H, R, E, P, payload):
@@ -54,39 +53,92 @@ def algorithmic_bytes(T, k, H, R, E, P, payload):
             "total": layout + dispatch + combine}
 
 
-# The source file that defines each kernel; every kernel also builds against epl_internal.h.
-KERNEL_SOURCES = {"route_hist_kernel": "layout.hip", "route_scan_kernel": "layout.hip",
-                  "route_finalize_kernel": "layout.hip", "route_single_kernel": "layout.hip",
-                  "dispatch_bf16_kernel": "dispatch.hip", "dispatch_fp8_kernel": "dispatch.hip",
-                  "combine_kernel": "combine.hip", "fused_bf16_kernel": "dispatch.hip"}
+
+LIB_PATH = os.path.join(ROOT, "paper_2607_06202_amd", "libepl.so")
+_BUNDLE_MAGIC = b"__CLANG_OFFLOAD_BUNDLE__"
 
 
-def source_hash(kernel):
-    """Hash of the code a kernel is built from: its source file and the shared header, with
-    comments and whitespace removed, so that a comment edit does not invalidate counter data."""
+def _elf_kernels(elf):
+    """(mangled name, code bytes, kernel descriptor bytes) of every kernel in one AMDGPU code
+    object (ELF64, little endian): the function symbols' bytes and their `.kd` objects."""
+    import struct
+
+    shoff, = struct.unpack_from("<Q", elf, 0x28)
+    shentsize, shnum = struct.unpack_from("<HH", elf, 0x3A)
+    secs = [struct.unpack_from("<IIQQQQIIQQ", elf, shoff + i * shentsize) for i in range(shnum)]
+    syms = {}
+    for sec in secs:
+        if sec[1] not in (2, 11):  # SHT_SYMTAB, SHT_DYNSYM
+            continue
+        strtab = secs[sec[6]]
+        for off in range(sec[4], sec[4] + sec[5], 24):
+            name_off, info, _, shndx, value, size = struct.unpack_from("<IBBHQQ", elf, off)
+            if shndx == 0 or shndx >= len(secs) or size == 0:
+                continue
+            start = strtab[4] + name_off
+            name = elf[start:elf.index(b"\0", start)].decode()
+            tgt = secs[shndx]
+            syms[name] = (info & 0xF, bytes(elf[tgt[4] + value - tgt[3]:tgt[4] + value - tgt[3] + size]))
+        break
+    out = []
+    for name, (typ, code) in syms.items():
+        if typ == 2 and name + ".kd" in syms:  # STT_FUNC with a kernel descriptor
+            kd = bytearray(syms[name + ".kd"][1])
+            kd[16:24] = bytes(8)  # entry offset: depends on where the kernel sits, not on its code
+            out.append((name, code, bytes(kd)))
+    return out
+
+
+def kernel_code_hashes(path=LIB_PATH):
+    """Hash of each kernel's gfx950 machine code and descriptor in a built library or object,
+    keyed by the kernel's unqualified name (template instances hashed together). Counter data
+    taken on a kernel stays valid exactly as long as this hash does."""
     import re
+    import struct
 
-    h = hashlib.sha256()
-    files = (KERNEL_SOURCES[kernel], "epl_internal.h") if kernel in KERNEL_SOURCES else sorted(
-        f for f in os.listdir(CSRC) if f.endswith((".hip", ".h")))
-    for f in files:
-        text = open(os.path.join(CSRC, f)).read()
-        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-        text = re.sub(r"//[^\n]*", " ", text)
-        h.update(f.encode())
-        h.update(" ".join(text.split()).encode())
-    return h.hexdigest()[:16]
+    data = open(path, "rb").read()
+    parts = {}
+    for m in re.finditer(re.escape(_BUNDLE_MAGIC), data):
+        b = m.start()
+        n, = struct.unpack_from("<Q", data, b + 24)
+        pos = b + 32
+        for _ in range(n):
+            off, size, tlen = struct.unpack_from("<QQQ", data, pos)
+            triple = data[pos + 24:pos + 24 + tlen].decode()
+            pos += 24 + tlen
+            if "amdgcn" in triple and "gfx950" in triple:
+                for name, code, kd in _elf_kernels(data[b + off:b + off + size]):
+                    mm = re.match(r"_ZN3epl(\d+)", name)
+                    base = name[mm.end():mm.end() + int(mm.group(1))] if mm else name
+                    parts.setdefault(base, []).append((name, code, kd))
+    hashes = {}
+    for base, items in parts.items():
+        h = hashlib.sha256()
+        for name, code, kd in sorted(items):
+            h.update(name.encode() + code + kd)
+        hashes[base] = h.hexdigest()[:16]
+    return hashes
+
+
+_CODE_HASHES = None
+
+
+def code_hash(kernel):
+    global _CODE_HASHES
+    if _CODE_HASHES is None:
+        _CODE_HASHES = kernel_code_hashes() if os.path.exists(LIB_PATH) else {}
+    return _CODE_HASHES.get(kernel)
 
 
 def load_traffic(kernel, workload):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were taken on the
-    current kernel sources; else None."""
+    kernel's current machine code; else None."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     ent = rec.get("kernels", {}).get("%s@%s" % (kernel, workload))
-    if not ent or ent.get("source_hash") != source_hash(kernel):
+    if not ent or ent.get("code_hash") is None or ent.get("code_hash") != code_hash(kernel):
         return None
     return ent.get("bytes_per_launch")
 
@@ -120,7 +172,7 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
         rec = {"kernels": {}}
     # Entries taken on older kernel sources no longer describe any kernel: drop them.
     rec["kernels"] = {k: v for k, v in rec.get("kernels", {}).items()
-                      if v.get("source_hash") == source_hash(k.split("@")[0])}
+                      if v.get("code_hash") is not None and v.get("code_hash") == code_hash(k.split("@")[0])}
     rec["calibration"] = {"fetch_factor": round(fetch_factor, 4), "write_factor": round(write_factor, 4),
                           "copy_bytes_each_way": int(n), "copy_fetch_kib": float(np.median(cf)),
                           "copy_write_kib": float(np.median(cw))}
@@ -129,16 +181,16 @@ def ingest_counters(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, worklo
              "calibration: 1 GiB device copy reads FETCH_SIZE %.1f KiB (factor %.4f), WRITE_SIZE %.1f KiB (factor %.4f)"
              % (np.median(cf), fetch_factor, np.median(cw), write_factor),
              "%-40s %8s %14s %14s %16s  %s" % ("kernel", "launches", "FETCH KiB", "WRITE KiB", "HBM bytes (cal.)",
-                                                "source hash")]
+                                                "code hash")]
     for name in fetch:
         if not name.startswith("epl::"):
             continue
         short = name.split("::")[1].split("<")[0]
         fk, wk = float(np.mean(fetch[name])), float(np.mean(write.get(name, [0.0])))
         b = fk * 1024 * fetch_factor + wk * 1024 * write_factor
-        rec["kernels"]["%s@%s" % (short, workload)] = {"source_hash": source_hash(short), "fetch_kib": fk,
+        rec["kernels"]["%s@%s" % (short, workload)] = {"code_hash": code_hash(short), "fetch_kib": fk,
                                                         "write_kib": wk, "bytes_per_launch": int(round(b))}
-        lines.append("%-40s %8d %14.1f %14.1f %16d  %s" % (name, len(fetch[name]), fk, wk, b, source_hash(short)))
+        lines.append("%-40s %8d %14.1f %14.1f %16d  %s" % (name, len(fetch[name]), fk, wk, b, code_hash(short)))
     json.dump(rec, open(TRAFFIC_FILE, "w"), indent=1, sort_keys=True)
     txt = os.path.join(ROOT, "profiles", "hbm_counters_%s.txt" % workload)
     open(txt, "w").write("\n".join(lines) + "\n")

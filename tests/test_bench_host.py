@@ -1,7 +1,6 @@
 """Host logic of bench.py (no GPU): the algorithmic byte counts behind the reported GB/s, the
-refusal of more than one GPU, and the source hash that keys committed counter data."""
+refusal of more than one GPU, and the machine-code hash that keys committed counter data."""
 import os
-import shutil
 import subprocess
 import sys
 
@@ -58,15 +57,42 @@ def test_more_than_one_gpu_is_refused():
     assert "single-GPU" in r.stderr
 
 
-def test_source_hash_ignores_comments_but_not_code(tmp_path, monkeypatch):
-    src = tmp_path / "csrc"
-    shutil.copytree(bench.CSRC, src)
-    monkeypatch.setattr(bench, "CSRC", str(src))
-    h0 = bench.source_hash("combine_kernel")
-    f = src / "combine.hip"
-    text = f.read_text()
-    f.write_text("// a new comment\n" + text.replace("\n", "\n   ", 3) + "\n/* block\n comment */\n")
-    assert bench.source_hash("combine_kernel") == h0
-    assert bench.source_hash("dispatch_bf16_kernel") != h0  # other file
-    f.write_text(text.replace("kGather = 8", "kGather = 4"))
-    assert bench.source_hash("combine_kernel") != h0
+def test_code_hash_follows_the_machine_code(tmp_path):
+    """The key of committed counter data is a hash of each kernel's gfx950 machine code and
+    descriptor, read from the built object: unchanged by a comment that shifts every source
+    line, changed by a change of code. (Compiles combine.hip three times with the library's
+    own flags; hipcc cross-compiles without a GPU.)"""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from paper_2607_06202_amd import _build
+
+    text = open(os.path.join(_build.CSRC, "combine.hip")).read()
+    variants = {"same": text,
+                "comment": "// a new comment\n/* and a block\n comment */\n" + text.replace("\n", "\n   ", 3),
+                "code": text.replace("kGather = 8", "kGather = 4")}
+    assert variants["code"] != text
+
+    def compile_variant(name):
+        src = tmp_path / ("%s.hip" % name)
+        src.write_text(variants[name])
+        obj = tmp_path / ("%s.o" % name)
+        subprocess.check_call([_build.HIPCC, *_build.FLAGS, "-I" + _build.CSRC, "-c", str(src), "-o", str(obj)])
+        return bench.kernel_code_hashes(str(obj))
+
+    with ThreadPoolExecutor(3) as ex:
+        h = dict(zip(variants, ex.map(compile_variant, variants)))
+    assert set(h["same"]) == {"combine_kernel", "debug_bf16_kernel"}
+    assert all(len(v) == 16 for v in h["same"].values())
+    assert h["comment"] == h["same"]
+    assert h["code"]["combine_kernel"] != h["same"]["combine_kernel"]
+    assert h["code"]["debug_bf16_kernel"] == h["same"]["debug_bf16_kernel"]
+
+
+def test_code_hashes_of_the_built_library():
+    """Every kernel of the library is found in its gfx950 code objects."""
+    if not os.path.exists(bench.LIB_PATH):
+        pytest.skip("libepl.so is not built")
+    h = bench.kernel_code_hashes()
+    assert {"route_hist_kernel", "route_scan_kernel", "route_finalize_kernel", "route_single_kernel",
+            "dispatch_bf16_kernel", "dispatch_fp8_kernel", "fused_bf16_kernel", "combine_kernel",
+            "locate_rows_kernel"} <= set(h)
