@@ -84,8 +84,18 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
   }
 }
 
+// Waves per SIMD of the plain bf16 kernel. The instance that reads a large x through buffer loads
+// is held at exactly 6; the other is left unconstrained (1 to 8, which compiles to the same code
+// as no attribute; its register use allows 8). Layout -> dispatch -> combine with the input
+// rotated, dispatch per call, two runs each, caps 3 / 4 / 6 / unconstrained:
+// * EP=32 prefill (buffer loads): 3278-3281 / 3242 / 3238-3242 / 3279-3280 us;
+// * EP=256 (buffer loads): 385.9-386.5 / 382.2-382.5 / 375.9-376.7 / 380.8-381.0 us;
+// * EP=64 decode (plain loads): 180.9-181.1 / 181.5 / 179.7-179.8 / 176.2-176.6 us.
+constexpr int bf16_min_waves(bool buf_x) { return buf_x ? 6 : 1; }
+constexpr int bf16_max_waves(bool buf_x) { return buf_x ? 6 : 8; }
 template <bool BUF_X>
 __global__ void __launch_bounds__(kDispatchThreads)
+    __attribute__((amdgpu_waves_per_eu(bf16_min_waves(BUF_X), bf16_max_waves(BUF_X))))
     dispatch_bf16_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
                          int64_t T, int k, int nv, int chunks, int64_t cap) {
   const int lane = threadIdx.x % kWave;
@@ -148,14 +158,17 @@ __device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, R
 
 // The fp8 kernel is capped at kFp8WavesPerSimd waves per SIMD. The compiler enforces the cap by
 // reserving a larger register budget. Each wave writes up to k scattered 1 KiB q rows per 2 KiB of
-// input, so fewer resident waves keep fewer concurrent random writes in flight. Skewed fp8 EP=64,
-// dispatch alone, input read from HBM:
-// * 8 waves (uncapped): 246.3 us;
-// * 4 waves: 244.5 us;
-// * 3 waves: 240.1 us;
-// * 2 waves: 234.2 us.
-// 1 wave per SIMD was about 30% slower than 2. The bf16 kernel measured best uncapped.
-constexpr int kFp8WavesPerSimd = 2;
+// input, so fewer resident waves keep fewer concurrent random writes in flight; too few leave the
+// per-element IEEE divisions of the quantiser exposed. Skewed fp8 EP=64, layout -> dispatch ->
+// combine with the input rotated, dispatch per call over three alternating runs each:
+// * 2 waves: 239.2-239.6 us;
+// * 3 waves: 209.2-209.7 us;
+// * 4 waves: 220.7-221.3 us;
+// * 6 waves: 222.6-223.4 us;
+// * 8 waves (uncapped): 222.6-222.8 us.
+// With 2 waves, multiplying by a reciprocal instead of dividing (not the defined rounding) also
+// brought it to 221 us, which places the 2-wave loss in the division latency.
+constexpr int kFp8WavesPerSimd = 3;
 __global__ void __launch_bounds__(kDispatchThreads) __attribute__((amdgpu_waves_per_eu(kFp8WavesPerSimd, kFp8WavesPerSimd)))
     dispatch_fp8_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
                         float* __restrict__ recv_scale, int64_t T, int k, int H, int npass, int64_t cap) {
