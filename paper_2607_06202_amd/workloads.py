@@ -289,6 +289,17 @@ WORKLOADS = {
 }
 WORKLOAD_ORDER = ["tiny", "decode_ep64", "prefill_ep32", "skewed_fp8_ep64", "large_ep256"]
 
+# The paper's other evaluated model shapes (its model-configuration table: hidden size, routed
+# experts, top-8) at decode batch sizes, and its default ablation setting (128 ranks, 64 tokens per
+# rank, one expert per rank), all with uniform routing and bf16 payloads.
+MODEL_WORKLOADS = {
+    "qwen3_30b_ep16": Workload("qwen3_30b_ep16", 16, 128, 8, 128, 2048, "bf16", "uniform"),
+    "glm47_ep32": Workload("glm47_ep32", 32, 160, 8, 128, 5120, "bf16", "uniform"),
+    "deepseek_ep128_bs64": Workload("deepseek_ep128_bs64", 128, 128, 8, 64, 7168, "bf16", "uniform"),
+}
+MODEL_ORDER = list(MODEL_WORKLOADS)
+WORKLOADS.update(MODEL_WORKLOADS)
+
 
 def routing(w: Workload, seed: int = 0) -> np.ndarray:
     """[T, k] int32 expert ids for a named workload."""

@@ -84,7 +84,7 @@ def test_layout_dispatch_all_invalid_and_empty(phases):
     _check(64, 256, 8, 0, 128, "bf16", 31, idx=np.zeros((0, 8), np.int32), phases=phases)
 
 
-@pytest.mark.parametrize("name", ["decode_ep64", "skewed_fp8_ep64", "large_ep256", "prefill_ep32"])
+@pytest.mark.parametrize("name", ["decode_ep64", "skewed_fp8_ep64", "large_ep256", "prefill_ep32"] + W.MODEL_ORDER)
 def test_layout_dispatch_matches_separate_calls_at_full_size(name):
     """The named workloads in the benchmark's configuration: the fused call, its two phases and
     epl_layout then epl_dispatch give identical layouts and identical payloads (compared on the

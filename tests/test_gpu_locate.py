@@ -14,7 +14,7 @@ from tests.gpu_util import device
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name", W.WORKLOAD_ORDER)
+@pytest.mark.parametrize("name", W.WORKLOAD_ORDER + W.MODEL_ORDER)
 def test_every_row_of_the_named_workloads(name):
     dev = device()
     w = W.WORKLOADS[name]

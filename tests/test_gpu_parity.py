@@ -143,7 +143,7 @@ def test_layout_empty_and_all_invalid():
     assert (out.float() == 0).all() and not torch.signbit(out.float()).any()  # +0 for tokens without pairs
 
 
-@pytest.mark.parametrize("name", W.WORKLOAD_ORDER)
+@pytest.mark.parametrize("name", W.WORKLOAD_ORDER + W.MODEL_ORDER)
 def test_layout_named_full_size(name):
     dev = device()
     w = W.WORKLOADS[name]
@@ -331,7 +331,7 @@ def _full_inputs(w, dev):
     return idx, x_d, gw
 
 
-@pytest.mark.parametrize("name", ["tiny", "decode_ep64", "prefill_ep32", "large_ep256"])
+@pytest.mark.parametrize("name", ["tiny", "decode_ep64", "prefill_ep32", "large_ep256"] + W.MODEL_ORDER)
 def test_bf16_full_size_round_trip_and_samples(name):
     dev = device()
     w = W.WORKLOADS[name]
