@@ -140,16 +140,33 @@ __device__ __forceinline__ int block_exclusive_sum(int v, int& total, int* scrat
 }
 
 // ---------------------------------------------------------------- number conversions
+// Clamp to [-448, 448], letting NaN through: the median of three returns -448 for a NaN.
+__device__ __forceinline__ float clamp_e4m3(float v) {
+  return __builtin_isnan(v) ? v : __builtin_amdgcn_fmed3f(v, 448.0f, -448.0f);
+}
+
+// Bit 7 of byte i set where the i-th value is a NaN with its sign bit clear (as an int32, a
+// positive NaN is above the bits of +Inf).
+__device__ __forceinline__ uint32_t positive_nan_bytes(float a, float b, float c, float d) {
+  uint32_t m = __float_as_int(a) > 0x7F800000 ? 0x00000080u : 0u;
+  m |= __float_as_int(b) > 0x7F800000 ? 0x00008000u : 0u;
+  m |= __float_as_int(c) > 0x7F800000 ? 0x00800000u : 0u;
+  m |= __float_as_int(d) > 0x7F800000 ? 0x80000000u : 0u;
+  return m;
+}
+
 // Four fp32 values -> four OCP E4M3 bytes (byte i from argument i), round to nearest even,
 // magnitudes above 448 saturated to 448 (the clamp is exact and RNE never rounds a value
-// below 464 past 448), sign kept on zero.
+// below 464 past 448), sign kept on zero, NaN -> 0x7F with its sign. The conversion instruction
+// writes 0xFF for every NaN, so the sign bit of a positive NaN's byte is cleared afterwards.
 __device__ __forceinline__ uint32_t f32x4_to_e4m3x4(float a, float b, float c, float d) {
-  a = __builtin_amdgcn_fmed3f(a, 448.0f, -448.0f);
-  b = __builtin_amdgcn_fmed3f(b, 448.0f, -448.0f);
-  c = __builtin_amdgcn_fmed3f(c, 448.0f, -448.0f);
-  d = __builtin_amdgcn_fmed3f(d, 448.0f, -448.0f);
+  const uint32_t pos_nan = positive_nan_bytes(a, b, c, d);
+  a = clamp_e4m3(a);
+  b = clamp_e4m3(b);
+  c = clamp_e4m3(c);
+  d = clamp_e4m3(d);
   const uint32_t lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0u, false);
-  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true) & ~pos_nan;
 }
 
 // Two fp32 -> packed bf16x2 (low half from `lo`), round to nearest even.

@@ -224,6 +224,68 @@ def test_dispatch_fp8_parity(R, E, k, Tr, H, seed):
     np.testing.assert_array_equal(scale.cpu().numpy().view(np.uint32), want_s.view(np.uint32))
 
 
+def _special_rows(H, n, seed):
+    """Rows whose 128-element blocks hold non-finite and extreme bf16 values: a NaN among normal
+    values, +Inf, -Inf with a NaN, only zeros of both signs, only subnormals, the largest finite
+    magnitude, only NaNs, and a lone tiny value."""
+    rng = np.random.default_rng(seed)
+    nan, pinf, ninf = 0x7FC1, 0x7F80, 0xFF80
+    rows = W.normal_bf16(seed, W.STREAM_X, n * H).reshape(n, H).copy()
+    for r in range(n):
+        blocks = rows[r].reshape(-1, 128)
+        for b in range(blocks.shape[0]):
+            kind = (b + r) % 8
+            blk = blocks[b]
+            if kind == 0:
+                blk[rng.integers(0, 128)] = nan | (0x8000 if r % 2 else 0)
+            elif kind == 1:
+                blk[rng.integers(0, 128)] = pinf
+            elif kind == 2:
+                blk[rng.integers(0, 128)] = ninf
+                blk[rng.integers(0, 128)] = nan
+            elif kind == 3:
+                blk[:] = np.where(rng.random(128) < 0.5, 0x0000, 0x8000)
+            elif kind == 4:
+                blk[:] = rng.integers(1, 0x80, 128) | np.where(rng.random(128) < 0.5, 0, 0x8000)
+            elif kind == 5:
+                blk[rng.integers(0, 128)] = 0x7F7F  # largest finite bf16
+            elif kind == 6:
+                blk[:] = nan | np.where(rng.random(128) < 0.5, 0, 0x8000)
+            else:
+                blk[:] = 0
+                blk[rng.integers(0, 128)] = 0x0001  # smallest subnormal
+    return rows.astype(np.uint16)
+
+
+@pytest.mark.parametrize("H", [1024, 1152])
+def test_dispatch_fp8_special_values(H):
+    """The quantiser on NaN, infinities, signed zeros, subnormals and the largest magnitude,
+    against the oracle. A block's amax ignores NaNs (so an all-NaN block gets s = 0, q = 0). With
+    an infinite amax the scale is +Inf; finite values then quantise to signed zeros and an
+    infinite value's quotient Inf/Inf is a NaN whose sign IEEE 754 leaves open, so for those
+    elements only the NaN code (low 7 bits 0x7F) is compared. Everything else is bit-exact."""
+    dev = device()
+    R, E, k, Tr = 2, 4, 3, 8
+    T = R * Tr
+    idx = W.with_replacement(11, T, k, 0, E).astype(np.int32)
+    x = _special_rows(H, T, 5)
+    w = W.Workload("sv", R, E, k, Tr, H, "fp8", "-")
+    cfg, L = run_layout(w, idx, dev)
+    recv, scale = epl.dispatch(cfg, to_dev_bf16(x, dev), L)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    want_q, want_s = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+    got_q, got_s = recv[:ref.P].cpu().numpy(), scale[:ref.P].cpu().numpy()
+    np.testing.assert_array_equal(got_s.view(np.uint32), want_s.view(np.uint32))
+    src = ref.recv_src
+    xi = x[src]  # the source row of every packed row
+    inf_quot = ((xi & 0x7FFF) == 0x7F80) & np.repeat(np.isinf(want_s), 128, axis=1)
+    exact = ~inf_quot
+    np.testing.assert_array_equal(got_q[exact], want_q[exact])
+    assert ((got_q[inf_quot] & 0x7F) == 0x7F).all() and ((want_q[inf_quot] & 0x7F) == 0x7F).all()
+    assert inf_quot.any() and np.isnan(oracle.bf16_to_f32(xi)).any()  # the cases are really there
+
+
 # ---------------------------------------------------------------------- combine
 @pytest.mark.parametrize("R,E,k,Tr,H,seed", [(4, 16, 2, 128, 256, 0), (3, 9, 5, 37, 264, 1), (8, 64, 8, 20, 7168, 2),
                                              (2, 2, 32, 9, 1032, 3), (16, 256, 9, 5, 520, 4)])
@@ -244,6 +306,42 @@ def test_combine_parity(R, E, k, Tr, H, seed):
     d = bf16_ulp_distance(got, want)
     assert d.max() <= 1, "combine off by %d ulp" % d.max()
     assert (got == want).all(), "combine within 1 ulp but %d elements not bit-exact" % (got != want).sum()
+
+
+def test_combine_special_values():
+    """Combine on expert rows with NaNs, infinities, signed zeros, subnormals and magnitudes whose
+    weighted sum overflows fp32 or rounds past the largest bf16, with zero, negative and
+    subnormal weights, against the oracle. Finite and infinite outputs are bit-exact; where the
+    output is a NaN only NaN-ness is compared, since IEEE 754 fixes no payload or sign for the
+    NaN an operation returns."""
+    dev = device()
+    R, E, k, Tr, H = 2, 8, 6, 64, 264
+    T = R * Tr
+    idx = W.with_replacement(21, T, k, -1, E + 1).astype(np.int32)
+    w = W.Workload("cs", R, E, k, Tr, H, "bf16", "-")
+    cfg, L = run_layout(w, idx, dev)
+    ref = oracle.layout(R, E, k, Tr, idx)
+    rng = np.random.default_rng(21)
+    y = W.normal_bf16(21, W.STREAM_Y, ref.P * H).reshape(ref.P, H).copy()
+    pick = rng.random(y.shape)
+    specials = np.array([0x7FC1, 0xFFC3, 0x7F80, 0xFF80, 0x0000, 0x8000, 0x0001, 0x807F, 0x7F7F, 0xFF7F, 0x7F00],
+                        np.uint16)
+    y = np.where(pick < 0.15, specials[rng.integers(0, specials.size, y.shape)], y).astype(np.uint16)
+    gw = W.softmax_gate_weights(21, T, k)
+    gw[::5] = 0.0
+    gw[1::7] *= -3.0
+    gw[2::11] = np.float32(1e-40)  # subnormal weight
+    gw[3::13] = np.float32(3.0)    # large weights push sums of big rows past the fp32 range
+    out = epl.combine(cfg, to_dev_bf16(y, dev), torch.from_numpy(gw).to(dev), L)
+    torch.cuda.synchronize()
+    want = oracle.combine(y, gw, ref.pair_row)
+    got = bf16_bits(out)
+    nan_w = np.isnan(oracle.bf16_to_f32(want))
+    nan_g = np.isnan(oracle.bf16_to_f32(got))
+    np.testing.assert_array_equal(nan_g, nan_w)
+    np.testing.assert_array_equal(got[~nan_w], want[~nan_w])
+    f = oracle.bf16_to_f32(want)
+    assert nan_w.any() and np.isinf(f).any() and (want == 0x8000).any()  # the cases are really there
 
 
 # ---------------------------------------------------------------------- randomised whole layers
