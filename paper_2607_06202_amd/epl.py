@@ -142,7 +142,26 @@ class Layout:
     workspace: torch.Tensor   # uint8 scratch
 
     def buffers(self) -> LayoutBuffers:
-        return LayoutBuffers(*[getattr(self, n).data_ptr() for n, _ in LayoutBuffers._fields_])
+        """The C struct of device pointers, built once and rebuilt only after a field is replaced."""
+        cached = self.__dict__.get("_buffers")
+        if cached is None:
+            cached = LayoutBuffers(*[getattr(self, n).data_ptr() for n, _ in LayoutBuffers._fields_])
+            object.__setattr__(self, "_buffers", cached)
+        return cached
+
+    def workspace_needed(self) -> int:
+        """epl_workspace_bytes of the layout's own config, computed once."""
+        need = self.__dict__.get("_ws_need")
+        if need is None:
+            need = workspace_bytes(self.cfg)
+            object.__setattr__(self, "_ws_need", need)
+        return need
+
+    def __setattr__(self, name, value):
+        super().__setattr__(name, value)
+        self.__dict__.pop("_buffers", None)
+        if name == "cfg":
+            self.__dict__.pop("_ws_need", None)
 
 
 def alloc_layout(cfg: Config, device) -> Layout:
@@ -191,8 +210,8 @@ def _layout_args(cfg: Config, topk_idx: torch.Tensor, out: Layout | None) -> Lay
         raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
     L = out if out is not None else alloc_layout(cfg, topk_idx.device)
     _check_layout(cfg, L, topk_idx.device)
-    if L.workspace.numel() < workspace_bytes(cfg):
-        raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), workspace_bytes(cfg)))
+    if L.workspace.numel() < L.workspace_needed():  # cfg has the layout's shape (checked above)
+        raise ValueError("layout workspace has %d bytes, needs %d" % (L.workspace.numel(), L.workspace_needed()))
     return L
 
 
