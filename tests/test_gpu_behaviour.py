@@ -29,26 +29,40 @@ def _inputs(R, E, k, Tr, H, seed, dev):
     return idx, x, gw, torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev), torch.from_numpy(gw).to(dev)
 
 
-def test_graph_capture_replays_match_eager():
-    """The three calls allocate nothing and issue no memsets, so they can be captured in a graph.
+@pytest.mark.parametrize("R,E,k,Tr,H,calls", [
+    (16, 64, 8, 24, 1024, "separate"),   # one-launch layout, then dispatch, combine
+    (64, 256, 8, 40, 1024, "fused"),     # counts, fused row kernel, combine, row location
+    (16, 512, 8, 256, 512, "phases"),    # three-launch layout then dispatch, as epl_layout_counts + epl_dispatch_rows
+])
+def test_graph_capture_replays_match_eager(R, E, k, Tr, H, calls):
+    """The calls allocate nothing and issue no memsets, so they can be captured in a graph.
     Replays with eager work in between must match the eager result every time."""
     dev = device()
-    R, E, k, Tr, H = 16, 64, 8, 24, 1024
     idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 3, dev)
     cfg = epl.config(R, E, k, H, Tr)
     L = epl.alloc_layout(cfg, dev)
     recv, _ = epl.alloc_recv(cfg, dev)
     out = torch.empty(R * Tr, H, dtype=torch.bfloat16, device=dev)
+    where = torch.empty(R * Tr * k, dtype=torch.int32, device=dev)
 
     def layer():
-        epl.layout(cfg, idx_d, out=L)
-        epl.dispatch(cfg, x_d, L, recv)
+        if calls == "separate":
+            epl.layout(cfg, idx_d, out=L)
+            epl.dispatch(cfg, x_d, L, recv)
+        elif calls == "fused":
+            epl.layout_dispatch(cfg, idx_d, x_d, out=L, recv=recv)
+        else:
+            epl.layout_counts(cfg, idx_d, out=L)
+            epl.dispatch_rows(cfg, idx_d, x_d, L, recv)
         epl.combine(cfg, recv, w_d, L, out)
+        e, _ = epl.locate_rows(cfg, L, n=R * Tr * k)
+        where.copy_(e)
 
     layer()
     torch.cuda.synchronize()
     want_rows = L.pair_row.clone()
     want_out = out.clone()
+    want_where = where.clone()
     s = torch.cuda.Stream(device=dev)
     s.wait_stream(torch.cuda.current_stream(dev))
     with torch.cuda.stream(s):
@@ -62,11 +76,13 @@ def test_graph_capture_replays_match_eager():
         L.pair_row.fill_(-5)
         out.zero_()
         recv.zero_()
+        where.fill_(-7)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(L.pair_row, want_rows), "replay %d: layout differs" % rep
         assert torch.equal(out.view(torch.int16), want_out.view(torch.int16)), "replay %d: combine differs" % rep
+        assert torch.equal(where, want_where), "replay %d: row location differs" % rep
         _ = (x_d.float() * 2).sum()  # unrelated eager work between replays
     ref = oracle.layout(R, E, k, Tr, idx)
     np.testing.assert_array_equal(want_rows.cpu().numpy(), ref.pair_row)
