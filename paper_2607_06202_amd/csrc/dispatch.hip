@@ -28,11 +28,11 @@ constexpr int64_t kBufferLoadXBytes = 200ll << 20;  // x at least this large: bu
 // Store one 16-byte vector at vector index v of a row of nv vectors through a buffer resource
 // scoped to that row, with an explicit cache policy. The resource bounds (nv * 16 bytes) also
 // guard the row. Measured on MI355X, layout -> dispatch -> combine back to back:
-// * bf16 rows: sc1 beat default-policy stores. Nontemporal stores were slower, because they
-//   make the dispatch pay its whole write cost before the next kernel can start.
-// * fp8 rows: sc1+nt beat both. The fp8 scales are partial-line writes of 32 bytes per row and
-//   pass. For them, plain stores measured faster than nontemporal ones (dispatch 235 -> 230 us,
-//   skewed fp8 EP=64).
+// * bf16 rows: sc1 beat default-policy stores (decode 175 against 179 us). Nontemporal stores
+//   were slower at every size: about +40 us at decode and EP=256, +105 us at prefill.
+// * fp8 rows: sc1+nt beat both (skewed fp8 EP=64: 207 us, against 246 us with sc1 and 252 us
+//   with default stores). The fp8 scales are partial-line writes of 32 bytes per row and pass;
+//   for them plain stores measured faster than nontemporal ones (235 -> 230 us).
 template <int POLICY>
 __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int nv, int v) {
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(row_base, 0, nv * 16, kBufferRsrcWord3);
