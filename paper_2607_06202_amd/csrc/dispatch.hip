@@ -211,8 +211,8 @@ hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* rec
 
 // ------------------------------------------------------------------------ layout finalize fused into dispatch
 // epl_layout_dispatch runs K1 and K2 of the layout, then one kernel that does both the layout's
-// finalize step and the dispatch. No workgroup waits on another; each dispatch wave works out the
-// rows of its own token from what K1 and K2 left in the workspace, with exactly the definitions
+// finalize step and the dispatch. No workgroup waits on another; the rows of each token are worked
+// out inside its workgroup from what K1 and K2 left in the workspace, with exactly the definitions
 // route_finalize_kernel applies to a whole chunk:
 // * row of pair (g, j) = first row of its expert (exclusive prefix of recv_cnt)
 //                      + rows of the expert before the token's chunk (K2's chunk offsets)
