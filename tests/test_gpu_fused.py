@@ -3,7 +3,8 @@ oracle: every layout output and the bf16 / fp8 payload, bit for bit. It takes th
 case asserts which one it exercises:
 * 3 launches, the layout's finalize step fused into the bf16 dispatch (at most 256 pairs per
   chunk and 256 experts): ragged last chunks, duplicates, invalid ids, 1 and 2 experts per rank,
-  more choices than experts;
+  more choices than experts, rows of 1, 2, 4 (ragged) and 5 column chunks, so that a
+  workgroup's waves cover four, two, one or parts of two tokens;
 * 4 launches, the layout then the dispatch (larger chunks, more experts, fp8);
 * 2 launches for small layouts."""
 import numpy as np
@@ -57,6 +58,9 @@ def _check(R, E, k, Tr, H, payload, seed, idx=None, phases=False):
     (64, 256, 8, 100, 8, 5, 3),      # 200 pairs per chunk; one 16-byte vector per row
     (16, 64, 8, 1024, 64, 6, 4),     # 512 pairs per chunk
     (8, 1024, 32, 1024, 64, 7, 4),   # k = 32, E = 1024
+    (64, 256, 8, 40, 4096, 8, 3),    # 2 column chunks per row: 2 tokens per workgroup
+    (32, 256, 8, 130, 6152, 9, 3),   # 4 chunks, the last one ragged (769 vectors per row)
+    (64, 256, 8, 40, 10240, 10, 3),  # 5 chunks: a workgroup's waves straddle two tokens
 ])
 @pytest.mark.parametrize("phases", [False, True])
 def test_layout_dispatch_bf16(R, E, k, Tr, H, seed, launches, phases):
