@@ -224,7 +224,7 @@ hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* rec
 // A workgroup's waves cover consecutive units, so they share few tokens (one when a row has as
 // many column chunks as the workgroup has waves). Wave w computes the rows of the workgroup's
 // w-th token, writes that token's pair_row, pair_rslot, recv_src and recv_j, and leaves the rows
-// in LDS for the other waves. A few extra workgroups at the end of the grid write expert_off,
+// in LDS for the other waves. A few extra workgroups at the start of the grid write expert_off,
 // rank_off and seg_off. The loads of x are issued before the row computation, so they are in
 // flight while it runs.
 struct FusedLayout {
@@ -378,10 +378,13 @@ __global__ void __launch_bounds__(kDispatchThreads)
     fused_bf16_kernel(FusedLayout F, const u32x4* __restrict__ x, u32x4* __restrict__ recv, int nv, int chunks,
                       int64_t cap, int unit_grid, int nmeta) {
   extern __shared__ int32_t lds[];
-  if ((int)blockIdx.x >= unit_grid) {
-    fused_meta_block(F, (int)blockIdx.x - unit_grid, nmeta, lds);
+  // The metadata workgroups come first in the grid, so that they run alongside the units
+  // instead of after them.
+  if ((int)blockIdx.x < nmeta) {
+    fused_meta_block(F, (int)blockIdx.x, nmeta, lds);
     return;
   }
+  const int blk = (int)blockIdx.x - nmeta;
   const int lane = threadIdx.x % kWave;
   const int w = threadIdx.x / kWave;
   const int k = F.G.k;
@@ -391,7 +394,7 @@ __global__ void __launch_bounds__(kDispatchThreads)
   const int64_t stride = (int64_t)unit_grid * kWavesPerBlock;
   // The loop bound depends on the workgroup's first unit only, so every wave runs the same
   // iterations and reaches the same barriers.
-  for (int64_t ub = (int64_t)blockIdx.x * kWavesPerBlock; ub < units; ub += stride) {
+  for (int64_t ub = (int64_t)blk * kWavesPerBlock; ub < units; ub += stride) {
     const int64_t g_first = ub / chunks;
     const int64_t g_last = std::min(units - 1, ub + kWavesPerBlock - 1) / chunks;
     const int64_t u = ub + w;
