@@ -41,6 +41,33 @@ def test_fused_row_kernel_bytes_add_the_placement_metadata():
     assert placement < b["layout"]  # the layout still accounts for them once in the total
 
 
+def test_per_rank_payload_matches_the_papers_bandwidth_table():
+    """Every bandwidth in the paper's EPCL table is one rank's dispatch payload divided by the
+    latency, with a payload of 7,340,032 bytes: 64 tokens x top-8 x 7168 x 2 bytes, one bf16 row
+    per (token, expert) pair. That is the payload term of this build's dispatch bytes, P*H*2 with
+    P = T*k, taken per rank at the paper's setting."""
+    path = os.path.join(os.path.dirname(__file__), "golden", "ep_comparison_latency_bw.txt")
+    rows = [list(map(int, ln.split())) for ln in open(path) if ln.strip() and not ln.startswith("#")]
+    assert len(rows) == 5
+    R, Tr, k, H = 128, 64, 8, 7168
+    b = bench.algorithmic_bytes(R * Tr, k, H, R, R, R * Tr * k, "bf16")
+    payload = (b["dispatch"] - R * Tr * H * 2 - R * Tr * k * 4) // R  # rows written per rank
+    assert payload == 64 * 8 * 7168 * 2 == 7_340_032
+    def consistent(nbytes, lat, bw):
+        # Latencies are printed to the microsecond and bandwidths to the GB/s: the bandwidth
+        # range the latency allows must meet the range the printed bandwidth stands for.
+        lo, hi = nbytes / ((lat + 0.5) * 1e3), nbytes / ((lat - 0.5) * 1e3)
+        return lo <= bw + 0.5 and hi >= bw - 0.5
+
+    for ep, lat_cann, bw_cann, lat_ubep, bw_ubep in rows:
+        for lat, bw in ((lat_cann, bw_cann), (lat_ubep, bw_ubep)):
+            assert consistent(payload, lat, bw), (ep, lat, bw)
+    # The table does not fit the byte counts of other plausible payloads: fp8 rows (half the
+    # bytes), or rows with the 56 fp32 scales of a 128-element block quantiser added.
+    for other in (payload // 2, payload + 64 * 8 * 56 * 4):
+        assert not all(consistent(other, lat, bw) for r in rows for lat, bw in ((r[1], r[2]), (r[3], r[4])))
+
+
 def test_fp8_bytes_include_one_scale_per_128_elements():
     b = _bytes("skewed_fp8_ep64")
     P, H = 16384 * 8, 7168
