@@ -12,7 +12,10 @@
 
 namespace epl {
 
-constexpr int kCombineThreads = 256;
+// Two waves per workgroup. Whole layer, two runs each, combine us with 128 / 256 / 512 threads:
+// decode 190.8-190.9 / 191.5-191.8 / 191.7-192.1; prefill 2875-2877 / 2897 / 2868;
+// skewed fp8 341.5-341.8 / 341.0 / 350; EP=256 365.8 / 366.0-367.2 / 363.2-363.4.
+constexpr int kCombineThreads = 128;
 constexpr int kCombineWaves = kCombineThreads / kWave;
 constexpr int kCombineCols = kWave;                  // one 16-byte vector per lane: 1 KiB of a row per unit
 constexpr int kGather = 8;                           // expert rows loaded before any is consumed

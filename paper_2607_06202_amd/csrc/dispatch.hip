@@ -18,8 +18,16 @@
 
 namespace epl {
 
-constexpr int kDispatchThreads = 256;
+constexpr int kDispatchThreads = 256;  // the fused kernel (its metadata workgroups scan with layout-sized blocks)
 constexpr int kWavesPerBlock = kDispatchThreads / kWave;
+// Workgroup sizes of the plain kernels. Whole layer, two runs each, dispatch us with 128 / 256 /
+// 512 threads: decode (bf16) 183.4-183.6 / 177.7-178.0 / 178.6-179.2; EP=256 (bf16) 396.8-397.1 /
+// 375.8-376.2 / 389.0-389.3; prefill (bf16) 3327 / 3239-3243 / 3282-3284; skewed fp8 202.3-203.2 /
+// 205.3-205.4 / 228.6.
+constexpr int kPlainThreads = 256;     // the plain bf16 dispatch kernel
+constexpr int kPlainWaves = kPlainThreads / kWave;
+constexpr int kFp8Threads = 128;       // the fp8 dispatch kernel
+constexpr int kFp8Waves = kFp8Threads / kWave;
 // bf16 work unit: one token's columns [u*kBf16Cols, (u+1)*kBf16Cols) in 16-byte vectors.
 constexpr int kBf16VPL = 4;                     // vectors per lane in one unit
 constexpr int kBf16Cols = kWave * kBf16VPL;     // 256 vectors = 4 KiB of a row
@@ -94,14 +102,14 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
 constexpr int bf16_min_waves(bool buf_x) { return buf_x ? 6 : 1; }
 constexpr int bf16_max_waves(bool buf_x) { return buf_x ? 6 : 8; }
 template <bool BUF_X>
-__global__ void __launch_bounds__(kDispatchThreads)
+__global__ void __launch_bounds__(kPlainThreads)
     __attribute__((amdgpu_waves_per_eu(bf16_min_waves(BUF_X), bf16_max_waves(BUF_X))))
     dispatch_bf16_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
                          int64_t T, int k, int nv, int chunks, int64_t cap) {
   const int lane = threadIdx.x % kWave;
   const int64_t units = T * chunks;
-  const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
-  for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
+  const int64_t stride = (int64_t)gridDim.x * kPlainWaves;
+  for (int64_t u = (int64_t)blockIdx.x * kPlainWaves + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / chunks;
     dispatch_bf16_unit<BUF_X>(
         x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
@@ -169,13 +177,13 @@ __device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, R
 // With 2 waves, multiplying by a reciprocal instead of dividing (not the defined rounding) also
 // brought it to 221 us, which places the 2-wave loss in the division latency.
 constexpr int kFp8WavesPerSimd = 3;
-__global__ void __launch_bounds__(kDispatchThreads) __attribute__((amdgpu_waves_per_eu(kFp8WavesPerSimd, kFp8WavesPerSimd)))
+__global__ void __launch_bounds__(kFp8Threads) __attribute__((amdgpu_waves_per_eu(kFp8WavesPerSimd, kFp8WavesPerSimd)))
     dispatch_fp8_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
                         float* __restrict__ recv_scale, int64_t T, int k, int H, int npass, int64_t cap) {
   const int lane = threadIdx.x % kWave;
   const int64_t units = T * npass;
-  const int64_t stride = (int64_t)gridDim.x * kWavesPerBlock;
-  for (int64_t u = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < units; u += stride) {
+  const int64_t stride = (int64_t)gridDim.x * kFp8Waves;
+  for (int64_t u = (int64_t)blockIdx.x * kFp8Waves + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / npass;
     dispatch_fp8_unit(x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, recv_scale, g,
                       (int)(u - g * npass), k, H, cap, lane);
@@ -188,12 +196,12 @@ hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* re
   const int nv = H / 8;
   const int chunks = (nv + kBf16Cols - 1) / kBf16Cols;
   const int64_t units = T * chunks;
-  const dim3 grid((unsigned)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30));
+  const dim3 grid((unsigned)std::min<int64_t>((units + kPlainWaves - 1) / kPlainWaves, 1 << 30));
   if (T * (int64_t)H * 2 >= kBufferLoadXBytes)
-    hipLaunchKernelGGL(dispatch_bf16_kernel<true>, grid, dim3(kDispatchThreads), 0, stream,
+    hipLaunchKernelGGL(dispatch_bf16_kernel<true>, grid, dim3(kPlainThreads), 0, stream,
                        static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
   else
-    hipLaunchKernelGGL(dispatch_bf16_kernel<false>, grid, dim3(kDispatchThreads), 0, stream,
+    hipLaunchKernelGGL(dispatch_bf16_kernel<false>, grid, dim3(kPlainThreads), 0, stream,
                        static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
   return hipGetLastError();
 }
@@ -203,8 +211,8 @@ hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* rec
   if (T == 0) return hipSuccess;
   const int npass = (H + 1023) / 1024;
   const int64_t units = T * npass;
-  const dim3 grid((unsigned)std::min<int64_t>((units + kWavesPerBlock - 1) / kWavesPerBlock, 1 << 30));
-  hipLaunchKernelGGL(dispatch_fp8_kernel, grid, dim3(kDispatchThreads), 0, stream, static_cast<const u32x4*>(x),
+  const dim3 grid((unsigned)std::min<int64_t>((units + kFp8Waves - 1) / kFp8Waves, 1 << 30));
+  hipLaunchKernelGGL(dispatch_fp8_kernel, grid, dim3(kFp8Threads), 0, stream, static_cast<const u32x4*>(x),
                      pair_row, static_cast<u32x4*>(recv), recv_scale, T, k, H, npass, cap);
   return hipGetLastError();
 }
