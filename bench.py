@@ -523,9 +523,12 @@ def main():
     kname = {"dispatch": "fused_bf16_kernel" if row_fused else
              "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
              "combine": "combine_kernel"}[dom]
+    traffic = load_traffic(kname, w.name)
     roofline = {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": load_traffic(kname, w.name), "algorithmic_bytes": dom_bytes,
+                "traffic": traffic, "algorithmic_bytes": dom_bytes,
+                # the counter bytes over the same duration: the HBM rate the kernel really moved
+                "traffic_GBps": None if traffic is None else round(traffic / (dom_us * 1e-6) / 1e9, 1),
                 "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev) if dev_ev else args.steps}
 
     cpu = None
