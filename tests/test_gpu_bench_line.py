@@ -28,6 +28,7 @@ def test_bench_json_line():
     roof = d["roofline"]
     assert roof["bound"] == "hbm" and roof["peak"] == 8000.0 and roof["unit"] == "GB/s"
     assert roof["achieved"] > 0 and abs(roof["frac"] - roof["achieved"] / roof["peak"]) < 1e-3
+    assert "traffic" in roof and "traffic_GBps" in roof
     assert roof["kernel"] in ("combine_kernel", "dispatch_bf16_kernel", "fused_bf16_kernel")
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["cores"] == 1 and cpu["value"] > 0 and cpu["sample"]
