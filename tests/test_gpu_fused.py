@@ -118,3 +118,26 @@ def test_layout_dispatch_matches_separate_calls_at_full_size(name):
         if s1p is not None:
             assert torch.equal(s1p.view(torch.int32), s2[:P].view(torch.int32)), what
         del L2, r2, s2
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_layout_dispatch_random_shapes(seed):
+    """Random shapes through epl_layout_dispatch and its two phases (alternating by seed):
+    ranks, experts per rank, k, tokens per rank, hidden sizes of 1 to 5 column chunks with ragged
+    tails, bf16 or fp8, with duplicates and invalid ids; every path the call can take appears."""
+    rng = np.random.default_rng(1300 + seed)
+    R = int(rng.choice([1, 4, 16, 32, 64, 128]))
+    El = int(rng.choice([1, 2, 4]))
+    E = R * El
+    k = int(rng.choice([1, 3, 8, 9]))
+    Tr = int(rng.choice([3, 16, 40, 100, 257]))
+    while R * Tr * k > 300_000:
+        Tr = max(1, Tr // 2)
+    payload = "fp8" if seed % 4 == 3 else "bf16"
+    H = int(rng.choice([128, 1152, 2176])) if payload == "fp8" else int(rng.choice([8, 1032, 2056, 4104, 9224]))
+    while R * Tr * k * H * 2 > 400_000_000:  # keep the host-side comparison small
+        Tr = max(1, Tr // 2)
+    lo, hi = (-1, E + 1) if seed % 2 else (0, E)
+    idx = W.with_replacement(seed, R * Tr, k, lo, hi).astype(np.int32)
+    _check(R, E, k, Tr, H, payload, seed, idx=idx, phases=bool(seed % 3 == 1))
+
