@@ -21,13 +21,14 @@
 //                      its stable rank among equal keys: ballot match over the key bits,
 //                      popcount of the lanes below, per-wave LDS running counts. A cross-wave
 //                      prefix then yields pair_row, recv_src, recv_j and pair_rslot.
+// For bf16 decode-sized layouts epl_layout_dispatch skips K3: the dispatch kernel derives each
+// token's rows from K1 and K2's workspace with the same definitions (dispatch.hip).
 //
 // Small integer quotients (pair -> token within a chunk, expert -> rank, seg_off index -> expert;
 // every numerator < 2^21) use small_div, which is exact in that range.
 #include "epl_internal.h"
 
 namespace epl {
-
 
 // Dedup of one token: bit j is set if pair j is valid (dt[j] >= 0) and no earlier valid pair of
 // the token targets the same destination rank dt[j].
