@@ -6,8 +6,8 @@ scatter (epl_layout_dispatch, or epl_layout then epl_dispatch with --separate), 
 gather-reduce (epl_combine), with identity experts in between (combine reads the receive buffer).
 Steps that carry timing events issue epl_layout_dispatch as its two phases, epl_layout_counts then
 epl_dispatch_rows (the same kernels), so that the row kernel is timed on its own. All inputs are
-resident in HBM before timing starts. The token matrix x is read from byte-identical copies in turn, at
-least 512 MB in total, so that no step finds its input in the 256 MB memory-side cache.
+resident in HBM before timing starts. The token matrix x is read from byte-identical copies in
+turn, at least 512 MB in total, so that no step finds its input in the 256 MB memory-side cache.
 
 Default workload: EP=64 decode. 64 virtual ranks, 256 experts (4 per rank), top-8, 128
 tokens per rank (8192 tokens), hidden 7168 bf16, uniform routing without replacement, softmax
@@ -51,7 +51,6 @@ def algorithmic_bytes(T, k, H, R, E, P, payload):
     # The row kernel with the layout's finalize step fused in also writes the placement metadata.
     return {"layout": layout, "dispatch": dispatch, "combine": combine, "rows_fused": dispatch + placement,
             "total": layout + dispatch + combine}
-
 
 
 LIB_PATH = os.path.join(ROOT, "paper_2607_06202_amd", "libepl.so")
