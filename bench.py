@@ -227,8 +227,33 @@ def device_info(torch):
                 info["max_package_power_w"] = int(open(cap[0]).read()) / 1e6  # microwatts
         except (OSError, ValueError):
             pass
+        info["temp_c"] = gpu_temperatures(dev)
+        info["_sysfs"] = dev
         break
     return info
+
+
+def device_end(info):
+    """The device fields for the output line, with the temperatures read again after the run."""
+    out = dict(info)
+    sysfs = out.pop("_sysfs", None)
+    out["temp_c_end"] = gpu_temperatures(sysfs) if sysfs else {}
+    return out
+
+
+def gpu_temperatures(dev_dir):
+    """The driver's temperature sensors of one GPU ({label: degrees C}, e.g. edge, junction,
+    mem), from its hwmon files; empty if there are none."""
+    import glob
+
+    temps = {}
+    for lab in sorted(glob.glob(os.path.join(dev_dir, "hwmon", "hwmon*", "temp*_label"))):
+        try:
+            name = open(lab).read().strip()
+            temps[name] = int(open(lab.replace("_label", "_input")).read()) / 1000.0  # millidegrees
+        except (OSError, ValueError):
+            pass
+    return temps
 
 
 def cpu_baseline(w, idx, x, gw, budget_s):
@@ -367,6 +392,7 @@ def main():
         return
 
     w = W.WORKLOADS[args.workload]
+    dinfo = device_info(torch)  # read before the run: the temperatures are those at the start
     if args.calibrate_replicate:
         calibrate_replicate(torch, epl, w, dev, stream, args.steps)
         return
@@ -551,7 +577,7 @@ def main():
         "us_layout_dispatch": round(us_dispatch + us_layout, 2),
         "us_combine": round(us_combine, 2),
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
-        "device": device_info(torch),
+        "device": device_end(dinfo),
         "launch": "graph" if graphs is not None else "eager",
         "calls": "epl_layout_dispatch + epl_combine" if args.fused else "epl_layout + epl_dispatch + epl_combine",
         "layout_dispatch_launches": launches,
