@@ -114,59 +114,53 @@ __global__ void __launch_bounds__(kLayoutThreads)
 }
 
 // ------------------------------------------------------------------------------------ K2
-constexpr int kScanNC = 16;  // chunks per source rank kept in registers (more go through a plain loop)
+constexpr int kScanNC = 16;  // rank rows: chunks kept in registers (more go through a plain loop)
+constexpr int kScanV = 4;    // expert columns: consecutive chunks per thread in one workgroup scan step
 
 __global__ void __launch_bounds__(kLayoutThreads)
     route_scan_kernel(Geom G, int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r,
                       const int32_t* __restrict__ inval, int32_t* __restrict__ recv_cnt, int32_t* __restrict__ send_cnt,
                       int32_t* __restrict__ rank_cnt, int32_t* __restrict__ seg_rel, int32_t* __restrict__ num_invalid) {
   __shared__ int32_t scratch[kLayoutWaves];
+  __shared__ int32_t seg_start[EPL_MAX_EXPERTS + 1];  // per source rank (R <= E), then the total
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   if (b < G.E) {
-    // Expert column e, laid out [source rank][chunk]: counts -> rows relative to the expert start.
+    // Expert column e, laid out [source rank][chunk] (flat index s * NC + c, the order of the
+    // expert's rows): an exclusive scan over the whole column gives each chunk's rows relative to
+    // the expert start. The workgroup scans kScanV consecutive chunks per thread at a time; the
+    // value at each rank's first chunk is that rank's segment start.
     const int e = b;
     int32_t* col = chunk_e + (int64_t)e * G.nblk;
-    const bool regs = G.NC <= kScanNC;  // uniform: the lane's NC counts fit in registers
     int carry = 0;
-    for (int s0 = 0; s0 < G.R; s0 += kLayoutThreads) {
-      const int s = s0 + tid;
-      const int sc = min(s, G.R - 1);
-      int h[kScanNC];
+    for (int base = 0; base < G.nblk; base += kLayoutThreads * kScanV) {
+      const int b0 = base + tid * kScanV;
+      int h[kScanV];
       int sum = 0;
-      if (regs) {
-        // All NC loads in flight together (index clamped into the lane's run), then one wait.
 #pragma unroll
-        for (int c = 0; c < kScanNC; ++c) h[c] = col[sc * G.NC + min(c, G.NC - 1)];
-#pragma unroll
-        for (int c = 0; c < kScanNC; ++c) sum += c < G.NC ? h[c] : 0;
-      } else {
-        for (int c = 0; c < G.NC; ++c) sum += col[sc * G.NC + c];
+      for (int v = 0; v < kScanV; ++v) {
+        h[v] = b0 + v < G.nblk ? col[b0 + v] : 0;
+        sum += h[v];
       }
-      if (s >= G.R) sum = 0;
       int total;
-      const int excl = block_exclusive_sum(sum, total, scratch);
-      if (s < G.R) {
-        const int base = carry + excl;
-        seg_rel[e * G.R + s] = base;
-        send_cnt[s * G.E + e] = sum;
-        int run = base;
-        if (regs) {
+      int run = carry + block_exclusive_sum(sum, total, scratch);
 #pragma unroll
-          for (int c = 0; c < kScanNC; ++c) {
-            if (c >= G.NC) break;
-            col[s * G.NC + c] = run;
-            run += h[c];
-          }
-        } else {
-          for (int c = 0; c < G.NC; ++c) {
-            const int hc = col[s * G.NC + c];
-            col[s * G.NC + c] = run;
-            run += hc;
-          }
+      for (int v = 0; v < kScanV; ++v) {
+        const int bb = b0 + v;
+        if (bb < G.nblk) {
+          col[bb] = run;
+          const int s = bb / G.NC;
+          if (bb == s * G.NC) seg_start[s] = run;
         }
+        run += h[v];
       }
       carry += total;
+    }
+    if (tid == 0) seg_start[G.R] = carry;
+    __syncthreads();
+    for (int s = tid; s < G.R; s += kLayoutThreads) {
+      seg_rel[e * G.R + s] = seg_start[s];
+      send_cnt[s * G.E + e] = seg_start[s + 1] - seg_start[s];
     }
     if (tid == 0) recv_cnt[e] = carry;
   } else if (b < G.E + G.R) {
