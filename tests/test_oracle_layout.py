@@ -124,6 +124,71 @@ def test_layout_exhaustive_micro(R, E, Tr, k, lo, hi):
     assert n == (hi - lo) ** (T * k)
 
 
+def brute_layout_batch(R, E, k, Tr, idx):
+    """The brute force over a batch of routing tables idx [N, T, k], in numpy: each table's pair
+    list stably sorted by expert id (argsort, kind="stable"), segment offsets counted as the pairs
+    that sort before (e, s), and each token's destination ranks as a boolean membership row."""
+    N, T, _ = idx.shape
+    El = E // R
+    e = idx.reshape(N, T * k).astype(np.int64)
+    valid = (e >= 0) & (e < E)
+    src = np.arange(T * k) // k // Tr
+    send_cnt = (valid[..., None] & (e[..., None] == np.arange(E))).reshape(N, R, Tr * k, E).sum(2)
+    expert_off = np.concatenate([np.zeros((N, 1), np.int64), np.cumsum(send_cnt.sum(1), 1)], 1)
+    ee, ss = np.arange(E)[:, None], np.arange(R)[None, :]
+    e4 = e[:, :, None, None]
+    before = (e4 < ee) | ((e4 == ee) & (src[None, :, None, None] < ss))
+    seg_off = (before & valid[:, :, None, None]).sum(1)
+    pos = np.arange(T * k)
+    order = np.argsort(np.where(valid, e, E), axis=1, kind="stable")
+    P = valid.sum(1)[:, None]
+    pair_row = np.empty((N, T * k), np.int64)
+    np.put_along_axis(pair_row, order, np.broadcast_to(pos, (N, T * k)), 1)
+    pair_row[~valid] = -1
+    d = np.where(valid, e // El, -1).reshape(N, T, k)
+    D = (d[..., None] == np.arange(R)).any(2)  # [N, T, R]: token g sends to rank r
+    Dr = D.reshape(N, R, Tr, R)
+    earlier = (np.cumsum(Dr, 2) - Dr).reshape(N, T, R)  # earlier tokens of the same source rank
+    slot = np.take_along_axis(earlier, np.maximum(d, 0), 2)
+    return dict(send_cnt=send_cnt, rank_cnt=Dr.sum(2), expert_off=expert_off, rank_off=expert_off[:, ::El],
+                seg_off=seg_off, tok_nranks=D.sum(2), pair_row=pair_row.reshape(N, T, k),
+                pair_rslot=np.where(d >= 0, slot, -1), recv_src=np.where(pos < P, order // k, -1),
+                recv_j=np.where(pos < P, order % k, -1), num_invalid=(~valid).sum(1))
+
+
+def test_layout_exhaustive_every_table():
+    """Every routing table of 2 ranks x 2 tokens, top-2 over 4 experts (2 per rank), with ids in
+    {-1, 0, 1, 2, 3}: 5^8 = 390,625 tables against the batched brute force."""
+    R, E, Tr, k = 2, 4, 2, 2
+    T = R * Tr
+    idx = (np.indices((5,) * (T * k)).reshape(T * k, -1).T - 1).astype(np.int32).reshape(-1, T, k)
+    N = idx.shape[0]
+    assert N == 5 ** 8
+    want = brute_layout_batch(R, E, k, Tr, idx)
+    sample = np.random.default_rng(5).choice(N, 300, replace=False)
+    for n in sample:  # the batched form agrees with the per-table brute force
+        one = brute_layout(R, E, k, Tr, idx[n])
+        for name, v in one.items():
+            w = want[name][n]
+            if name in ("recv_src", "recv_j"):
+                w = w[:len(v)]
+            np.testing.assert_array_equal(np.asarray(w).reshape(np.shape(v)), v, err_msg=name)
+    got = {name: np.full(v.shape, -9, np.int64) for name, v in want.items()}
+    for n in range(N):
+        L = oracle.layout(R, E, k, Tr, idx[n])
+        for name in ("send_cnt", "rank_cnt", "expert_off", "rank_off", "seg_off", "tok_nranks", "pair_row",
+                     "pair_rslot"):
+            got[name][n] = getattr(L, name)
+        P = L.recv_src.size
+        got["recv_src"][n, :P] = L.recv_src
+        got["recv_j"][n, :P] = L.recv_j
+        got["recv_src"][n, P:] = got["recv_j"][n, P:] = -1
+        got["num_invalid"][n] = L.num_invalid
+    for name, v in want.items():
+        bad = np.flatnonzero((got[name] != v).reshape(N, -1).any(1))
+        assert bad.size == 0, "%s differs on %d tables, e.g. %s" % (name, bad.size, idx[bad[0]].tolist())
+
+
 # ------------------------------------------------------------------ randomised shapes
 @pytest.mark.parametrize("seed", range(12))
 def test_layout_random_vs_brute(seed):
