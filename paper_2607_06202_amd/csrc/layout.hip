@@ -114,8 +114,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
 }
 
 // ------------------------------------------------------------------------------------ K2
-constexpr int kScanNC = 16;  // rank rows: chunks kept in registers (more go through a plain loop)
-constexpr int kScanV = 4;    // expert columns: consecutive chunks per thread in one workgroup scan step
+constexpr int kScanV = 4;  // consecutive elements per thread in one workgroup scan step
 
 __global__ void __launch_bounds__(kLayoutThreads)
     route_scan_kernel(Geom G, int32_t* __restrict__ chunk_e, int32_t* __restrict__ chunk_r,
@@ -164,30 +163,44 @@ __global__ void __launch_bounds__(kLayoutThreads)
     }
     if (tid == 0) recv_cnt[e] = carry;
   } else if (b < G.E + G.R) {
-    // Source rank s: per destination rank r, slots of earlier chunks come first.
+    // Source rank s: per destination rank r, slots of earlier chunks come first. The rank's
+    // [chunk][R] block of counts is scanned as one flat sequence in (r, chunk) order, so each r
+    // is a contiguous segment; an element's slot base is the flat exclusive prefix minus the
+    // prefix at its segment's first chunk.
     const int s = b - G.E;
     int32_t* rows = chunk_r + (int64_t)s * G.NC * G.R;  // this rank's NC chunk rows of R counts
-    for (int r = tid; r < G.R; r += kLayoutThreads) {
-      int run = 0;
-      if (G.NC <= kScanNC) {
-        int h[kScanNC];
+    const int n = G.NC * G.R;
+    int carry = 0;
+    for (int base = 0; base < n; base += kLayoutThreads * kScanV) {
+      int h[kScanV], at[kScanV], rr[kScanV];
+      int sum = 0;
 #pragma unroll
-        for (int c = 0; c < kScanNC; ++c) h[c] = rows[(int64_t)min(c, G.NC - 1) * G.R + r];
-#pragma unroll
-        for (int c = 0; c < kScanNC; ++c) {
-          if (c >= G.NC) break;
-          rows[(int64_t)c * G.R + r] = run;
-          run += h[c];
-        }
-      } else {
-        for (int c = 0; c < G.NC; ++c) {
-          const int hc = rows[(int64_t)c * G.R + r];
-          rows[(int64_t)c * G.R + r] = run;
-          run += hc;
-        }
+      for (int v = 0; v < kScanV; ++v) {
+        const int f = base + tid * kScanV + v;
+        rr[v] = f / G.NC;
+        const int c = f - rr[v] * G.NC;
+        at[v] = f < n ? c * G.R + rr[v] : -1;
+        h[v] = f < n ? rows[at[v]] : 0;
+        sum += h[v];
       }
-      rank_cnt[s * G.R + r] = run;
+      int total;
+      int run = carry + block_exclusive_sum(sum, total, scratch);
+      int pre[kScanV];
+#pragma unroll
+      for (int v = 0; v < kScanV; ++v) {
+        pre[v] = run;
+        if (at[v] >= 0 && at[v] < G.R) seg_start[rr[v]] = run;  // chunk 0 of rank rr[v]
+        run += h[v];
+      }
+      carry += total;
+      __syncthreads();  // segment starts found in this step are visible
+#pragma unroll
+      for (int v = 0; v < kScanV; ++v)
+        if (at[v] >= 0) rows[at[v]] = pre[v] - seg_start[rr[v]];
     }
+    if (tid == 0) seg_start[G.R] = carry;
+    __syncthreads();
+    for (int r = tid; r < G.R; r += kLayoutThreads) rank_cnt[s * G.R + r] = seg_start[r + 1] - seg_start[r];
   } else {
     int n = 0;
     for (int i = tid; i < G.nblk; i += kLayoutThreads) n += inval[i];
