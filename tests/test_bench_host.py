@@ -44,7 +44,7 @@ def test_fused_row_kernel_bytes_add_the_placement_metadata():
 def test_per_rank_payload_matches_the_papers_bandwidth_table():
     """Every bandwidth in the paper's EPCL table is one rank's dispatch payload divided by the
     latency, with a payload of 7,340,032 bytes: 64 tokens x top-8 x 7168 x 2 bytes, one bf16 row
-    per (token, expert) pair. That is the payload term of this build's dispatch bytes, P*H*2 with
+    per (token, expert) pair. That is the payload term of the bench's dispatch byte model, P*H*2 with
     P = T*k, taken per rank at the paper's setting."""
     path = os.path.join(os.path.dirname(__file__), "golden", "ep_comparison_latency_bw.txt")
     rows = [list(map(int, ln.split())) for ln in open(path) if ln.strip() and not ln.startswith("#")]
