@@ -3,6 +3,7 @@
 * bitwise determinism of dispatch and combine;
 * no stores past the P packed rows at full size;
 * non-default streams;
+* combine writing its output over x;
 * the paper's other model shapes: Qwen3-30B (hidden 2048, 128 experts), GLM-4.7 (hidden 5120,
   160 routed experts) and DeepSeek at 128 ranks, from the model-configuration table and the
   end-to-end deployments.
@@ -148,6 +149,29 @@ def test_side_stream_dispatch_and_combine():
     rr = oracle.dispatch_bf16(x, ref.pair_row, ref.P)
     np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), rr)
     np.testing.assert_array_equal(bf16_bits(out), oracle.combine(rr, gw, ref.pair_row))
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_combine_output_over_x(fused):
+    """epl_combine may write its output over x (dispatch is done with it, on the same stream). With
+    identity experts and softmax weights the layer then leaves x's own storage holding x again, and
+    the packed rows are untouched."""
+    dev = device()
+    R, E, k, Tr, H = 64, 256, 8, 24, 1024
+    idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 12, dev)
+    cfg = epl.config(R, E, k, H, Tr)
+    if fused:
+        L, recv, _ = epl.layout_dispatch(cfg, idx_d, x_d)
+    else:
+        L = epl.layout(cfg, idx_d)
+        recv, _ = epl.dispatch(cfg, x_d, L)
+    ptr = x_d.data_ptr()
+    out = epl.combine(cfg, recv, w_d, L, out=x_d)
+    torch.cuda.synchronize()
+    assert out.data_ptr() == ptr
+    assert torch.equal(x_d.float(), to_dev_bf16(x, dev).float())  # +0 == -0: a -0 input comes back as +0
+    ref = oracle.layout(R, E, k, Tr, idx)
+    np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), oracle.dispatch_bf16(x, ref.pair_row, ref.P))
 
 
 @pytest.mark.parametrize("name,R,E,H,Tr", [("qwen3_30b_ep16", 16, 128, 2048, 64), ("glm47_ep32", 32, 160, 5120, 16),
