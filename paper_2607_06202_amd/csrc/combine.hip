@@ -1,7 +1,7 @@
 // MoE combine on one GPU: gate-weighted gather-reduce of expert output rows back into token order
 // (the paper's combine: gather expert outputs and restore the original token order).
 //
-// Work is cut into equal units, each a (token, 1 KiB column chunk) pair, one unit per wave. The
+// Work is cut into equal units, each a (token, column chunk) pair, one unit per wave. The
 // workgroup stages its tokens' k packed-row indices and k gate weights in LDS with one coalesced
 // load. A wave issues the 16-byte loads of up to 8 expert rows before consuming any (many
 // gathers in flight). It then folds them in the token's own j order, acc = fmaf(w_j, y_j, acc),
@@ -17,30 +17,41 @@ namespace epl {
 // skewed fp8 341.5-341.8 / 341.0 / 350; EP=256 365.8 / 366.0-367.2 / 363.2-363.4.
 constexpr int kCombineThreads = 128;
 constexpr int kCombineWaves = kCombineThreads / kWave;
-constexpr int kCombineCols = kWave;                  // one 16-byte vector per lane: 1 KiB of a row per unit
 constexpr int kGather = 8;                           // expert rows loaded before any is consumed
+// Column chunk of a unit: VPL 16-byte vectors per lane, so 1 KiB (VPL = 1) or 2 KiB (VPL = 2) of each
+// of the token's rows.
+template <int VPL>
+constexpr int combine_cols() { return kWave * VPL; }
 
 // One unit: gather chunk c of the token's k expert rows and fold them in j order. Row
 // indices and weights are wave-uniform and are read into scalar registers, so skipping an
 // invalid pair is a scalar branch. With k <= kGather all loads are issued before the first
 // fmaf. Larger k walks the choices in groups of kGather, still in j order.
-template <bool SMALL_K>
+template <bool SMALL_K, int VPL>
 __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const int32_t* rows, const float* ws,
                                              u32x4* __restrict__ out, int64_t g, int c, int k, int nv, int lane) {
-  const int v = c * kCombineCols + lane;
-  const bool on = v < nv;
-  const int vl = min(v, nv - 1);  // clamped so the gather loads need no per-lane branch
-  float acc[8];
+  int v[VPL], vl[VPL];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+  for (int q = 0; q < VPL; ++q) {
+    v[q] = c * combine_cols<VPL>() + q * kWave + lane;
+    vl[q] = min(v[q], nv - 1);  // clamped so the gather loads need no per-lane branch
+  }
+  float acc[VPL][8];
+#pragma unroll
+  for (int q = 0; q < VPL; ++q)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[q][e] = 0.0f;
   const int kend = SMALL_K ? kGather : k;
   for (int j0 = 0; j0 < kend; j0 += kGather) {
-    u32x4 buf[kGather];
+    u32x4 buf[kGather][VPL];
 #pragma unroll
     for (int jj = 0; jj < kGather; ++jj) {
       const int j = j0 + jj;
       const int row = j < k ? __builtin_amdgcn_readfirstlane(rows[j]) : -1;
-      if (row >= 0) buf[jj] = __builtin_nontemporal_load(y + (int64_t)row * nv + vl);
+      if (row >= 0) {
+#pragma unroll
+        for (int q = 0; q < VPL; ++q) buf[jj][q] = __builtin_nontemporal_load(y + (int64_t)row * nv + vl[q]);
+      }
     }
 #pragma unroll
     for (int jj = 0; jj < kGather; ++jj) {
@@ -49,20 +60,26 @@ __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const 
       if (row < 0) continue;
       const float wj = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, ws[j])));
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[2 * i] = fmaf(wj, bf16lo_to_f32(buf[jj][i]), acc[2 * i]);
-        acc[2 * i + 1] = fmaf(wj, bf16hi_to_f32(buf[jj][i]), acc[2 * i + 1]);
+      for (int q = 0; q < VPL; ++q) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc[q][2 * i] = fmaf(wj, bf16lo_to_f32(buf[jj][q][i]), acc[q][2 * i]);
+          acc[q][2 * i + 1] = fmaf(wj, bf16hi_to_f32(buf[jj][q][i]), acc[q][2 * i + 1]);
+        }
       }
     }
   }
-  if (on) {
-    u32x4 o;
+  // Streamed stores through a resource bounded to the output row, device scope (sc1) and
+  // nontemporal: they leave no dirty lines behind and measured best of the store policies.
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(out + g * nv, 0, nv * 16, kBufferRsrcWord3);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = f32x2_to_bf16x2(acc[2 * i], acc[2 * i + 1]);
-    // Streamed store through a resource bounded to the output row, device scope (sc1) and
-    // nontemporal: it leaves no dirty lines behind and measured best of the store policies.
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(out + g * nv, 0, nv * 16, kBufferRsrcWord3);
-    __builtin_amdgcn_raw_buffer_store_b128(o, rs, v * 16, 0, kCachePolicySc1Nt);
+  for (int q = 0; q < VPL; ++q) {
+    if (v[q] < nv) {
+      u32x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = f32x2_to_bf16x2(acc[q][2 * i], acc[q][2 * i + 1]);
+      __builtin_amdgcn_raw_buffer_store_b128(o, rs, v[q] * 16, 0, kCachePolicySc1Nt);
+    }
   }
 }
 
@@ -77,10 +94,20 @@ __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const 
 // * EP=32 prefill: 3066 -> 2927 us;
 // * skewed fp8: 371 -> 345 us.
 // 3 waves per SIMD measured within 1% of 4. 2 waves per SIMD was too few to cover the latency.
-constexpr int kCombineWavesPerSimd = 4;
-template <bool SMALL_K>
+//
+// For a receive buffer of prefill size the wide form is used: 2 KiB column chunks at 2 waves per
+// SIMD, the same bytes in flight per CU as 1 KiB at 4 waves but half as many concurrent read
+// streams. Whole layer, two alternating runs each, combine us, 1 KiB at 4 waves against 2 KiB at
+// 2 / 3 / 4 waves:
+// * EP=32 prefill (15 GB of y): 2893-2896 against 2876 / 2977-2979 / 3041;
+// * EP=256 (1.9 GB): 367.3-367.4 against 366.6-367.2 / 386-387 / 391-392;
+// * skewed fp8 (1.9 GB): 342.3-343.2 against 343.2-344.6 / 365 / 371;
+// * EP=64 decode (0.9 GB): 190.6-196.4 against 194.1-194.4 / 200 / 201.
+constexpr int combine_waves_per_simd(int vpl) { return vpl == 1 ? 4 : 2; }
+constexpr int64_t kWideCombineBytes = 4ll << 30;  // T*k*H*2 (the bound on y) from which the wide form runs
+template <bool SMALL_K, int VPL>
 __global__ void __launch_bounds__(kCombineThreads)
-    __attribute__((amdgpu_waves_per_eu(kCombineWavesPerSimd, kCombineWavesPerSimd)))
+    __attribute__((amdgpu_waves_per_eu(combine_waves_per_simd(VPL), combine_waves_per_simd(VPL))))
     combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ w, const int32_t* __restrict__ pair_row,
                    u32x4* __restrict__ out, int64_t T, int k, int nv, int chunks) {
   __shared__ int32_t rows_lds[kCombineWaves * EPL_MAX_TOPK];
@@ -100,26 +127,35 @@ __global__ void __launch_bounds__(kCombineThreads)
     const int64_t unit = ub + threadIdx.x / kWave;
     if (unit >= units) continue;
     const int64_t g = unit / chunks;
-    combine_unit<SMALL_K>(y, rows_lds + (g - g_first) * k, w_lds + (g - g_first) * k, out, g,
+    combine_unit<SMALL_K, VPL>(y, rows_lds + (g - g_first) * k, w_lds + (g - g_first) * k, out, g,
                           (int)(unit - g * chunks), k, nv, lane);
   }
+}
+
+template <int VPL>
+void launch_combine_vpl(const u32x4* y, const float* w, const int32_t* pair_row, u32x4* out, int64_t T, int k, int nv,
+                        hipStream_t stream) {
+  const int chunks = (nv + combine_cols<VPL>() - 1) / combine_cols<VPL>();
+  const int64_t blocks = (T * chunks + kCombineWaves - 1) / kCombineWaves;
+  const dim3 grid((unsigned)std::min<int64_t>(blocks, 1 << 30));
+  if (k <= kGather)
+    hipLaunchKernelGGL((combine_kernel<true, VPL>), grid, dim3(kCombineThreads), 0, stream, y, w, pair_row, out, T, k,
+                       nv, chunks);
+  else
+    hipLaunchKernelGGL((combine_kernel<false, VPL>), grid, dim3(kCombineThreads), 0, stream, y, w, pair_row, out, T, k,
+                       nv, chunks);
 }
 
 hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
                           int H, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const int nv = H / 8;
-  const int chunks = (nv + kCombineCols - 1) / kCombineCols;
-  const int64_t blocks = (T * chunks + kCombineWaves - 1) / kCombineWaves;
-  const dim3 grid((unsigned)std::min<int64_t>(blocks, 1 << 30));
   const u32x4* yv = static_cast<const u32x4*>(y);
   u32x4* ov = static_cast<u32x4*>(out);
-  if (k <= kGather)
-    hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(kCombineThreads), 0, stream, yv, w, pair_row, ov, T, k, nv,
-                       chunks);
+  if (T * k * (int64_t)H * 2 >= kWideCombineBytes)
+    launch_combine_vpl<2>(yv, w, pair_row, ov, T, k, nv, stream);
   else
-    hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(kCombineThreads), 0, stream, yv, w, pair_row, ov, T, k, nv,
-                       chunks);
+    launch_combine_vpl<1>(yv, w, pair_row, ov, T, k, nv, stream);
   return hipGetLastError();
 }
 
