@@ -340,6 +340,8 @@ def main():
                          "epl_layout_dispatch + epl_combine")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP graph replays of the layer (one graph per x copy) instead of eager launches")
+    ap.add_argument("--recv-alloc", choices=["contiguous", "torch"], default="contiguous",
+                    help="receive buffer: one physically contiguous HIP block (default) or torch's allocator")
     ap.add_argument("--warm", action="store_true",
                     help="read the same x every step (it may stay in the memory-side cache) instead of rotating copies")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
@@ -411,7 +413,16 @@ def main():
     xs = [x_d] + [x_d.clone() for _ in range(n_x - 1)]
     w_d = torch.from_numpy(gw).to(dev)
     L = epl.alloc_layout(cfg, dev)
-    recv, recv_scale = epl.alloc_recv(cfg, dev)
+    # The receive rows as one physically contiguous block, as a serving process would allocate them
+    # once (torch's allocator if the driver has no such block, or with --recv-alloc torch).
+    recv_alloc = args.recv_alloc
+    if recv_alloc == "contiguous":
+        try:
+            recv, recv_scale = epl.alloc_recv(cfg, dev, contiguous=True)
+        except MemoryError:
+            recv_alloc = "torch"
+    if recv_alloc == "torch":
+        recv, recv_scale = epl.alloc_recv(cfg, dev)
     out = torch.empty(w.T, w.H, dtype=torch.bfloat16, device=dev)
     if w.payload == "fp8":
         # combine reads bf16 expert outputs; identity experts would dequantise -- here a bf16
@@ -583,7 +594,7 @@ def main():
         "layout_dispatch_launches": launches,
         "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
         "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,
-        "roofline": roofline, "x_copies": n_x, "x_reuse": "warm" if args.warm else "rotated",
+        "roofline": roofline, "x_copies": n_x, "x_reuse": "warm" if args.warm else "rotated", "recv_alloc": recv_alloc,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec))

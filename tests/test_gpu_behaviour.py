@@ -4,6 +4,7 @@
 * no stores past the P packed rows at full size;
 * non-default streams;
 * combine writing its output over x;
+* the receive buffer as one contiguous HIP block;
 * the paper's other model shapes: Qwen3-30B (hidden 2048, 128 experts), GLM-4.7 (hidden 5120,
   160 routed experts) and DeepSeek at 128 ranks, from the model-configuration table and the
   end-to-end deployments.
@@ -172,6 +173,53 @@ def test_combine_output_over_x(fused):
     assert torch.equal(x_d.float(), to_dev_bf16(x, dev).float())  # +0 == -0: a -0 input comes back as +0
     ref = oracle.layout(R, E, k, Tr, idx)
     np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), oracle.dispatch_bf16(x, ref.pair_row, ref.P))
+
+
+@pytest.mark.parametrize("payload", ["bf16", "fp8"])
+def test_contiguous_receive_buffer(payload):
+    """alloc_recv(contiguous=True): the payload rows live in one HIP block handed to torch. The
+    layer on it matches the oracle."""
+    dev = device()
+    R, E, k, Tr, H = 16, 64, 4, 20, 1024
+    idx, x, gw, idx_d, x_d, w_d = _inputs(R, E, k, Tr, H, 13, dev)
+    cfg = epl.config(R, E, k, H, Tr, payload)
+    recv, scale = epl.alloc_recv(cfg, dev, contiguous=True)
+    assert recv.shape == (R * Tr * k, H) and recv.device == dev and recv.is_contiguous()
+    assert recv.dtype == (torch.uint8 if payload == "fp8" else torch.bfloat16)
+    L = epl.layout(cfg, idx_d)
+    epl.dispatch(cfg, x_d, L, recv, scale)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    if payload == "bf16":
+        np.testing.assert_array_equal(bf16_bits(recv[:ref.P]), oracle.dispatch_bf16(x, ref.pair_row, ref.P))
+        out = epl.combine(cfg, recv, w_d, L)
+        torch.cuda.synchronize()
+        assert torch.equal(out.float(), x_d.float())
+    else:
+        q, sc = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+        np.testing.assert_array_equal(recv[:ref.P].cpu().numpy(), q)
+        np.testing.assert_array_equal(scale[:ref.P].cpu().numpy().view(np.uint32), sc.view(np.uint32))
+
+
+def test_contiguous_block_lives_as_long_as_its_tensors():
+    """torch keeps the HIP block alive while a tensor (or a view of one) uses it, and the block is
+    freed once the last one is gone."""
+    import gc
+    import weakref
+    dev = device()
+    b = epl._ContiguousBlock(64 << 20, dev)
+    t = b.tensor((1 << 15, 1024), torch.bfloat16)
+    v = t[7:9]
+    alive = weakref.ref(b)
+    del b, t
+    gc.collect()
+    assert alive() is not None, "the block was dropped while a view still uses it"
+    v.fill_(3.0)
+    torch.cuda.synchronize()
+    assert bool((v.float() == 3.0).all())
+    del v
+    gc.collect()
+    assert alive() is None, "the block outlived its tensors"
 
 
 @pytest.mark.parametrize("name,R,E,H,Tr", [("qwen3_30b_ep16", 16, 128, 2048, 64), ("glm47_ep32", 32, 160, 5120, 16),
