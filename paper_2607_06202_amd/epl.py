@@ -276,8 +276,17 @@ class _ContiguousBlock:
             self.ptr = ctypes.c_void_p()
             raise MemoryError("no physically contiguous block of %d bytes on %s (hip status %d)" %
                               (nbytes, self.device, rc))
+        self.nbytes = nbytes
 
     def tensor(self, shape, dtype: torch.dtype) -> torch.Tensor:
+        """A tensor over the start of the block; its extent must fit in the block (the kernels
+        write wherever a tensor says its rows are)."""
+        n = dtype.itemsize
+        for d in shape:
+            n *= int(d)
+        if n > self.nbytes:
+            raise ValueError("a %s tensor of shape %s needs %d bytes; the block has %d" %
+                             (dtype, tuple(shape), n, self.nbytes))
         typestr = {torch.bfloat16: "<i2", torch.uint8: "|u1"}[dtype]
         self.__cuda_array_interface__ = {"shape": tuple(shape), "typestr": typestr, "strides": None,
                                          "data": (self.ptr.value, False), "version": 2}

@@ -223,3 +223,17 @@ def test_config_rules_property(lib, R, E, k, H, Tr, payload):
         st_ = call_layout(lib, c)
         assert st_ in (INVALID, UNSUPPORTED)
         assert (st_ == UNSUPPORTED) == (payload not in (0, 1) and _valid(R, E, k, H, Tr, 0))
+
+
+def test_contiguous_block_views_must_fit_the_block():
+    """A tensor over a contiguous HIP block may not claim more bytes than the block holds: the
+    kernels write wherever the tensor says its rows are. The check runs on the host, before any
+    memory is touched (an object without a device allocation stands in for the block here)."""
+    import torch
+
+    b = object.__new__(epl._ContiguousBlock)
+    b.ptr, b.nbytes, b.device = ctypes.c_void_p(), 100, torch.device("cuda:0")
+    with pytest.raises(ValueError):
+        b.tensor((51,), torch.bfloat16)  # 102 bytes
+    with pytest.raises(ValueError):
+        b.tensor((3, 34), torch.uint8)  # 102 bytes
