@@ -419,7 +419,7 @@ def main():
     if recv_alloc == "contiguous":
         try:
             recv, recv_scale = epl.alloc_recv(cfg, dev, contiguous=True)
-        except MemoryError:
+        except (MemoryError, OSError):  # no contiguous block free, or the HIP runtime not found by name
             recv_alloc = "torch"
     if recv_alloc == "torch":
         recv, recv_scale = epl.alloc_recv(cfg, dev)
