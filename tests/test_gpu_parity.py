@@ -462,6 +462,46 @@ def test_bf16_full_size_round_trip_and_samples(name):
     assert (got == want).all(), name + ": sampled combine not bit-exact"
 
 
+def test_wide_combine_large_k_and_ragged_chunk():
+    """The wide combine form (2 KiB column chunks, taken from 4 GiB of expert rows) with k = 13,
+    so the choices are folded in two groups of gathers, and H = 20,488, so the last column chunk
+    holds a single vector: 8 ranks of 1,024 tokens give T*k*H*2 = 4.36 GB. Sampled tokens (the
+    first and last among them) against the oracle, on the dispatched rows and on independent
+    expert rows."""
+    dev = device()
+    R, E, k, Tr, H = 8, 64, 13, 1024, 20488
+    T = R * Tr
+    assert T * k * H * 2 >= 4 << 30 and (H // 8) % 128 == 1
+    idx = W.distinct_uniform(5, np.arange(T), k, E).astype(np.int32)
+    idx[::101, 4] = -1  # a few invalid pairs
+    x_d = W.device_normal_bf16((T, H), seed=3, device=dev)
+    gw = W.softmax_gate_weights(5, T, k)
+    cfg = epl.config(R, E, k, H, Tr)
+    idx_d = torch.from_numpy(idx).to(dev)
+    L, recv, _ = epl.layout_dispatch(cfg, idx_d, x_d)
+    w_d = torch.from_numpy(gw).to(dev)
+    out = epl.combine(cfg, recv, w_d, L)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    assert_layout_equal(L, ref, "wide combine case")
+    # the dispatched rows as expert outputs (tokens with an invalid pair do not get x back)
+    rng = np.random.default_rng(3)
+    toks = np.unique(np.concatenate([rng.integers(0, T, 96), [0, T - 1]]))
+    need = np.unique(ref.pair_row[toks][ref.pair_row[toks] >= 0])
+    row_map = np.full(ref.P, -1, np.int32)
+    row_map[need] = np.arange(need.size)
+    sel = torch.from_numpy(need.astype(np.int64)).to(dev)
+    want = oracle.combine_mapped(bf16_bits(recv[sel]), row_map, gw, ref.pair_row, toks)
+    got = bf16_bits(out[torch.from_numpy(toks).to(dev)])
+    np.testing.assert_array_equal(got, want)
+    # independent expert rows
+    y = W.device_normal_bf16((ref.P, H), seed=8, device=dev)
+    out2 = epl.combine(cfg, y, w_d, L)
+    torch.cuda.synchronize()
+    want2 = oracle.combine_mapped(bf16_bits(y[sel]), row_map, gw, ref.pair_row, toks)
+    np.testing.assert_array_equal(bf16_bits(out2[torch.from_numpy(toks).to(dev)]), want2)
+
+
 def test_fp8_full_size_skewed():
     dev = device()
     w = W.WORKLOADS["skewed_fp8_ep64"]
