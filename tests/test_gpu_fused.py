@@ -141,3 +141,30 @@ def test_layout_dispatch_random_shapes(seed):
     idx = W.with_replacement(seed, R * Tr, k, lo, hi).astype(np.int32)
     _check(R, E, k, Tr, H, payload, seed, idx=idx, phases=bool(seed % 3 == 1))
 
+
+
+def test_fused_row_kernel_with_buffer_loads():
+    """An x of 200 MB or more is read through buffer loads, in the fused row kernel as in the
+    plain dispatch: 64 ranks of 100 tokens at H = 16,384 (210 MB of x, chunks of 25 tokens, so the
+    finalize step is still fused). The layout against the oracle; every packed row against its
+    source row, bit for bit."""
+    dev = device()
+    R, E, k, Tr, H = 64, 256, 8, 100, 16384
+    T = R * Tr
+    cfg = epl.config(R, E, k, H, Tr)
+    assert T * H * 2 >= 200 << 20 and epl.layout_dispatch_launches(cfg) == 3
+    idx = W.distinct_uniform(21, np.arange(T), k, E).astype(np.int32)
+    idx[::37, 2] = -1
+    x_d = W.device_normal_bf16((T, H), seed=21, device=dev)
+    for phases in (False, True):
+        if phases:
+            L = epl.layout_counts(cfg, torch.from_numpy(idx).to(dev))
+            recv, _ = epl.dispatch_rows(cfg, torch.from_numpy(idx).to(dev), x_d, L)
+        else:
+            L, recv, _ = epl.layout_dispatch(cfg, torch.from_numpy(idx).to(dev), x_d)
+        torch.cuda.synchronize()
+        ref = oracle.layout(R, E, k, Tr, idx)
+        assert_layout_equal(L, ref, "fused, buffer loads, phases=%s" % phases)
+        src = torch.from_numpy(ref.recv_src.astype(np.int64)).to(dev)
+        assert torch.equal(recv[:ref.P].view(torch.int16), x_d[src].view(torch.int16))
+        del L, recv
