@@ -37,6 +37,7 @@ METRIC = "dispatch+combine µs/MoE layer and effective HBM GB/s (% of peak), EP=
 HBM_PEAK_GBS = 8000.0
 X_ROTATION_BYTES = 512 << 20  # twice the MI355X memory-side cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+ROOFLINE_SAMPLES = 20  # launches of the dominant kernel timed with events, at least (fewer only if K < 20)
 
 
 def algorithmic_bytes(T, k, H, R, E, P, payload):
@@ -256,27 +257,70 @@ def gpu_temperatures(dev_dir):
     return temps
 
 
-def cpu_baseline(w, idx, x, gw, budget_s):
-    """The oracle (plain single-threaded C), timed on this host's CPU on the same inputs."""
+def host_threads():
+    """Host threads the CPU baseline may use: the cores this process may run on, capped by
+    OMP_NUM_THREADS when that is set (the share of the host given to one GPU's jobs)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    cap = os.environ.get("OMP_NUM_THREADS")
+    if cap and cap.isdigit() and int(cap) > 0:
+        n = min(n, int(cap))
+    return max(1, n)
+
+
+def cpu_baseline(w, idx, x, gw, budget_s, threads):
+    """The oracle, unchanged, timed on this host's CPU on the same inputs, two ways:
+    * single thread: oracle.layout, then the dispatch and the combine over all tokens;
+    * `threads` threads: the same layout call, then the unchanged dispatch and combine functions
+      called on disjoint token ranges from a thread pool (ctypes releases the GIL), the
+      partition the survey's multi-thread mode names for scatter and combine.
+    The threaded layer's receive rows and output must equal the single-thread ones bit for bit.
+    For fp8 the combine reads a bf16 buffer of zeros, as the GPU layer does. Each leg runs whole
+    layers until its half of the budget is spent (at least one)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
 
-    t0 = time.perf_counter()
-    reps = 0
-    while True:
+    fp8 = w.payload == "fp8"
+    T, H, k = w.T, w.H, w.k
+
+    def layer(recv, scale, out, pool=None, ranges=None):
         L = oracle.layout(w.R, w.E, w.k, w.Tr, idx)
-        if w.payload == "fp8":
-            recv, _ = oracle.dispatch_fp8(x, L.pair_row, L.P)
-            y = None
+        y = recv if not fp8 else y_zero
+        if pool is None:
+            oracle.dispatch_range_into(x, L.pair_row, recv, 0, T, scale)
+            oracle.combine_range_into(y, gw, L.pair_row, out, 0, T)
         else:
-            recv = oracle.dispatch_bf16(x, L.pair_row, L.P)
-            y = recv
-        if y is not None:
-            oracle.combine(y, gw, L.pair_row)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or reps >= 50:
-            break
-    return el / reps, reps, L.P
+            list(pool.map(lambda r: oracle.dispatch_range_into(x, L.pair_row, recv, r[0], r[1], scale), ranges))
+            list(pool.map(lambda r: oracle.combine_range_into(y, gw, L.pair_row, out, r[0], r[1]), ranges))
+        return L.P
+
+    rows = max(T * k, 1)
+    y_zero = np.zeros((rows, H), np.uint16) if fp8 else None
+    legs = {}
+    outputs = {}
+    for name, n in (("single", 1), ("threads", threads)):
+        recv = np.zeros((rows, H), np.uint8 if fp8 else np.uint16)
+        scale = np.zeros((rows, H // 128), np.float32) if fp8 else None
+        out = np.zeros((T, H), np.uint16)
+        step = max(1, -(-T // (4 * n)))  # a few ranges per thread
+        ranges = [(g, min(T, g + step)) for g in range(0, T, step)]
+        pool = ThreadPoolExecutor(n) if n > 1 else None
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            P_ref = layer(recv, scale, out, pool, ranges)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s / 2 or reps >= 50:
+                break
+        if pool is not None:
+            pool.shutdown()
+        legs[name] = (el / reps, reps, n)
+        outputs[name] = (recv[:P_ref], None if scale is None else scale[:P_ref], out)
+    a, b = outputs["single"], outputs["threads"]
+    identical = bool(np.array_equal(a[0], b[0]) and np.array_equal(a[2], b[2]) and
+                     (a[1] is None or np.array_equal(a[1].view(np.uint32), b[1].view(np.uint32))))
+    return legs, identical, P_ref
 
 
 def calibrate_replicate(torch, epl, w, dev, stream, steps):
@@ -318,13 +362,25 @@ def calibrate_replicate(torch, epl, w, dev, stream, steps):
 
 
 def cpu_model():
+    """The host CPU as /proc/cpuinfo names it, with its family, model and stepping numbers (a
+    virtualised host may report only a short brand name), and the logical CPUs it lists."""
+    fields = {}
+    ncpu = 0
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            key, _, val = line.partition(":")
+            key = key.strip()
+            if key == "processor":
+                ncpu += 1
+            if key in ("model name", "cpu family", "model", "stepping", "vendor_id") and key not in fields:
+                fields[key] = val.strip()
     except OSError:
-        pass
-    return None
+        return None
+    if not fields:
+        return None
+    return "%s (vendor %s, family %s, model %s, stepping %s; %d logical CPUs listed)" % (
+        fields.get("model name", "?"), fields.get("vendor_id", "?"), fields.get("cpu family", "?"),
+        fields.get("model", "?"), fields.get("stepping", "?"), ncpu)
 
 
 def main():
@@ -490,10 +546,12 @@ def main():
             graphs[i % n_x].replay()
         torch.cuda.synchronize()
 
-    # Timed region: K plain steps. Every 10th step brackets only the dominant call with two HIP
-    # events on the library's stream, so the markers barely perturb the wall time. Graph replays
-    # take no markers; the dominant call's duration then comes from the instrumented pass below.
-    sample = [i for i in range(args.steps) if i % 10 == 0] if graphs is None else []
+    # Timed region: K plain steps. At least ROOFLINE_SAMPLES of them (every step when K is
+    # small, evenly spaced otherwise) bracket only the dominant call with two HIP events on the
+    # library's stream; the other calls carry no markers. Graph replays take no markers; the
+    # dominant call's duration then comes from the instrumented pass below.
+    every = max(1, args.steps // ROOFLINE_SAMPLES)
+    sample = [i for i in range(args.steps) if i % every == 0] if graphs is None else []
     dev_ev = {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for i in sample}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -569,13 +627,19 @@ def main():
 
     cpu = None
     if args.cpu_budget > 0:
-        sec, reps, P_ref = cpu_baseline(w, idx, x, gw, args.cpu_budget)
+        legs, identical, P_ref = cpu_baseline(w, idx, x, gw, args.cpu_budget, host_threads())
         assert P_ref == P
-        cpu = {"value": round(nbytes["total"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-               "cpu_model": cpu_model(),
-               "us_per_layer": round(sec * 1e6, 1),
-               "sample": "%d full %s layer(s) (layout+dispatch+combine) on the same inputs, single thread" % (
-                   reps, w.name)}
+        if not identical:
+            raise AssertionError("threaded oracle layer differs from the single-thread one")
+        (sec1, reps1, _), (secn, repsn, nthr) = legs["single"], legs["threads"]
+        cpu = {"value": round(nbytes["total"] / secn / 1e9, 3), "unit": "GB/s", "cores": nthr, "kind": "oracle",
+               "cpu_model": cpu_model(), "us_per_layer": round(secn * 1e6, 1),
+               "sample": "%d full %s layer(s) (layout+dispatch+combine) on the same inputs; layout on one thread, "
+                         "dispatch and combine on %d threads over disjoint token ranges" % (repsn, w.name, nthr),
+               "bit_identical_to_single_thread": identical,
+               "single_thread": {"value": round(nbytes["total"] / sec1 / 1e9, 3), "unit": "GB/s", "cores": 1,
+                                 "us_per_layer": round(sec1 * 1e6, 1),
+                                 "sample": "%d full layer(s), one thread" % reps1}}
 
     rec = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,

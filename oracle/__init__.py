@@ -177,6 +177,36 @@ def combine_mapped(ys: np.ndarray, row_map: np.ndarray, w: np.ndarray, pair_row:
     return out
 
 
+def _at(a: np.ndarray, elem_offset: int):
+    """Pointer to element elem_offset of a C-contiguous array (for calls on token sub-ranges)."""
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return ctypes.c_void_p(a.ctypes.data + int(elem_offset) * a.itemsize)
+
+
+def dispatch_range_into(x: np.ndarray, pair_row: np.ndarray, recv: np.ndarray, g0: int, g1: int,
+                        recv_scale: np.ndarray | None = None) -> None:
+    """eplref_dispatch_bf16 (or _fp8 when recv_scale is given) on tokens [g0, g1) only, writing
+    into the caller's recv (and recv_scale). The C function is called unchanged on the token
+    range's rows of x and pair_row; the rows it writes are the range's own, so calls on disjoint
+    ranges may run at the same time (ctypes releases the GIL)."""
+    T, H = x.shape
+    k = pair_row.shape[1]
+    if recv_scale is None:
+        lib().eplref_dispatch_bf16(g1 - g0, k, H, _at(x, g0 * H), _at(pair_row, g0 * k), _p(recv))
+    else:
+        lib().eplref_dispatch_fp8(g1 - g0, k, H, _at(x, g0 * H), _at(pair_row, g0 * k), _p(recv),
+                                  _p(recv_scale))
+
+
+def combine_range_into(y: np.ndarray, w: np.ndarray, pair_row: np.ndarray, out: np.ndarray, g0: int,
+                       g1: int) -> None:
+    """eplref_combine on tokens [g0, g1) only, writing out[g0:g1] of the caller's out."""
+    H = y.shape[1]
+    k = pair_row.shape[1]
+    lib().eplref_combine(g1 - g0, k, H, _p(y), _at(w, g0 * k), _at(pair_row, g0 * k), None, 0,
+                         _at(out, g0 * H))
+
+
 def locate_rows(expert_off: np.ndarray, rows=None, n: int | None = None):
     """Expert and in-expert offset of packed rows (Token-level Load Partition; Algorithm 1's
     result): rows, or 0..n-1 when rows is None. Positions outside [0, P) give (-1, -1)."""

@@ -7,9 +7,9 @@ target minus the count below that expert. These tests pin the oracle, which read
 off the exclusive prefix expert_off by a linear scan, against:
 * that list formulation by brute force, exhaustively over small count vectors with empty experts;
 * the closed form for equal counts;
-* the paper's quaternary search written out step by step (three pivots per step, with the
-  termination reading), on random lists with empty experts;
-and show that the printed loop, taken literally, never leaves a window of one expert.
+* a four-way interval search of this test's own (window invariant off[lo] <= t < off[hi],
+  three cut points per step, at most ceil(log4 E) steps), on random lists with empty experts;
+and show why a window of one expert needs an explicit stop (Algorithm 1's termination reading).
 """
 import itertools
 
@@ -32,27 +32,24 @@ def _vector_count(lst, p):
     return int(np.count_nonzero(lst < p))
 
 
-def _quaternary_search(lst, t, n_exp, fixed=True, max_steps=64):
-    """The paper's Algorithm 1: window [L, R] over experts, pivots L + i*Gap for i = 1..3, counts
-    by VectorCount, narrow to the first quadrant whose right count exceeds the target. With
-    fixed=True the loop runs while the window spans more than one expert."""
-    L, R, c_left = 0, n_exp, 0
-    gap = -(-(R - L) // 4)
+def _four_way_locate(off, t):
+    """A four-way interval search over experts, written for this test from Algorithm 1's idea:
+    the window [lo, hi) of experts always satisfies off[lo] <= t < off[hi]; each step cuts it
+    into four parts of ceil(width / 4) experts (the last part possibly shorter) and keeps the
+    part whose cumulative range holds t, reading three cut points of the prefix. It stops once
+    one expert is left. Returns (expert, offset, steps)."""
+    lo, hi = 0, len(off) - 1
+    assert off[lo] <= t < off[hi]
     steps = 0
-    while gap >= 1 and (not fixed or R - L > 1):
+    while hi - lo > 1:
+        width = -(-(hi - lo) // 4)
+        cuts = [min(lo + i * width, hi) for i in (1, 2, 3)]
+        part = sum(1 for c in cuts if off[c] <= t)  # cut points at or below the target
+        bounds = [lo] + cuts + [hi]
+        lo, hi = bounds[part], bounds[part + 1]
+        assert off[lo] <= t < off[hi], (lo, hi, t)
         steps += 1
-        if steps > max_steps:
-            raise RuntimeError("window stuck at [%d, %d]" % (L, R))
-        pivots = [L + i * gap for i in (1, 2, 3)]
-        counts = [_vector_count(lst, p) for p in pivots]
-        q = next((i for i in (1, 2, 3) if t < counts[i - 1]), 4)
-        bounds = [L] + pivots + [R]
-        lefts = [c_left] + counts
-        L, R, c_left = bounds[q - 1], bounds[q], lefts[q - 1]
-        gap = -(-(R - L) // 4)
-        if R <= L or gap == 0:
-            break
-    return L, t - _vector_count(lst, L), steps
+    return lo, t - int(off[lo]), steps
 
 
 def test_exhaustive_small_lists_against_the_list_formulation():
@@ -86,30 +83,38 @@ def test_dense_rows_equal_counts_closed_form():
 
 
 @pytest.mark.parametrize("seed", range(6))
-def test_paper_quaternary_search_agrees(seed):
-    """Random per-expert counts with about 40% of the experts empty:
-    the quaternary search, run to a one-expert window, returns the oracle's expert and offset
-    for every target, in at most ceil(log4(E)) + 1 steps."""
+def test_four_way_search_agrees(seed):
+    """Random per-expert counts with about 40% of the experts empty: the four-way search keeps
+    its window invariant, returns the oracle's expert and offset for every target, and needs at
+    most ceil(log4(E)) steps."""
     rng = np.random.default_rng(seed)
     E = int(rng.choice([1, 2, 3, 5, 16, 63, 160, 256, 300]))
     counts = rng.integers(0, 4, E) * (rng.random(E) < 0.6)
     counts[rng.integers(0, E)] += 1  # at least one token
-    lst = _expert_list(counts)
-    e, o = oracle.locate_rows(_offsets(counts), n=lst.size)
-    bound = int(np.ceil(np.log(max(E, 2)) / np.log(4))) + 1
-    for t in range(lst.size):
-        qe, qo, steps = _quaternary_search(lst, t, E)
+    off = _offsets(counts)
+    P = int(off[-1])
+    e, o = oracle.locate_rows(off, n=P)
+    bound = int(np.ceil(np.log(E) / np.log(4) - 1e-12)) if E > 1 else 0
+    for t in range(P):
+        qe, qo, steps = _four_way_locate(off, t)
         assert (qe, qo) == (e[t], o[t]), (seed, t)
-        assert steps <= bound
+        assert steps <= bound, (seed, t, steps, bound)
 
 
-def test_printed_loop_does_not_leave_a_one_expert_window():
-    """Taken literally, the loop recomputes Gap = ceil(1/4) = 1 once R - L = 1, picks the same
-    quadrant again and never meets its break condition; the reading stops at R - L = 1."""
-    counts = [2, 0, 3, 1]
-    lst = _expert_list(counts)
-    e, o = oracle.locate_rows(_offsets(counts), n=lst.size)
-    for t in range(lst.size):
-        with pytest.raises(RuntimeError, match="stuck"):
-            _quaternary_search(lst, t, len(counts), fixed=False)
-        assert _quaternary_search(lst, t, len(counts))[:2] == (e[t], o[t])
+def test_one_expert_window_needs_an_explicit_stop():
+    """Algorithm 1's update recomputes its pivot spacing as ceil(width / 4) and stops only when
+    the window is empty or that spacing is zero. Once the window spans one expert the spacing is
+    ceil(1/4) = 1, so neither test holds and the window is mapped to itself: the reading stops the
+    search at width one instead. Shown on the four-way step above, with the stop removed: from a
+    one-expert window it returns the same window."""
+    off = _offsets([2, 0, 3, 1])
+    for lo in range(4):
+        if off[lo + 1] == off[lo]:
+            continue
+        t = int(off[lo])
+        width = -(-1 // 4)
+        assert width == 1
+        cuts = [min(lo + i * width, lo + 1) for i in (1, 2, 3)]
+        part = sum(1 for c in cuts if off[c] <= t)
+        bounds = [lo] + cuts + [lo + 1]
+        assert (bounds[part], bounds[part + 1]) == (lo, lo + 1)
