@@ -37,7 +37,7 @@ METRIC = "dispatch+combine µs/MoE layer and effective HBM GB/s (% of peak), EP=
 HBM_PEAK_GBS = 8000.0
 X_ROTATION_BYTES = 512 << 20  # twice the MI355X memory-side cache
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-ROOFLINE_SAMPLES = 20  # launches of the dominant kernel timed with events, at least (fewer only if K < 20)
+ROOFLINE_SAMPLES = 20  # launches of the dominant kernel timed with HIP events, at least
 
 
 def algorithmic_bytes(T, k, H, R, E, P, payload):
@@ -391,6 +391,9 @@ def main():
     ap.add_argument("--workload", default="decode_ep64")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time (0 to skip)")
+    ap.add_argument("--roofline-samples", type=int, default=ROOFLINE_SAMPLES,
+                    help="launches of the dominant call timed with HIP events, at least: every 10th timed step, "
+                         "topped up by steps right after the timed region")
     ap.add_argument("--separate", action="store_true",
                     help="time epl_layout, epl_dispatch and epl_combine as three calls instead of "
                          "epl_layout_dispatch + epl_combine")
@@ -546,41 +549,56 @@ def main():
             graphs[i % n_x].replay()
         torch.cuda.synchronize()
 
-    # Timed region: K plain steps. At least ROOFLINE_SAMPLES of them (every step when K is
-    # small, evenly spaced otherwise) bracket only the dominant call with two HIP events on the
-    # library's stream; the other calls carry no markers. Graph replays take no markers; the
-    # dominant call's duration then comes from the instrumented pass below.
-    every = max(1, args.steps // ROOFLINE_SAMPLES)
-    sample = [i for i in range(args.steps) if i % every == 0] if graphs is None else []
-    dev_ev = {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for i in sample}
+    def run_steps(first, n, dev_ev):
+        """n plain steps starting at step index `first`; the steps in dev_ev bracket only the
+        dominant call with two HIP events on the library's stream."""
+        for i in range(first, first + n):
+            if graphs is not None:
+                graphs[i % n_x].replay()
+                continue
+            ev = dev_ev.get(i)
+            if args.fused and not (ev is not None and dom == "dispatch"):
+                epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
+            else:
+                if args.fused:
+                    epl.layout_counts(cfg, idx_d, out=L)
+                else:
+                    epl.layout(cfg, idx_d, out=L)
+                if ev is not None:
+                    ev[0].record(stream)
+                if args.fused:
+                    epl.dispatch_rows(cfg, idx_d, xs[i % n_x], L, recv, recv_scale)
+                else:
+                    epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
+            if ev is not None:
+                ev[1 if dom == "dispatch" else 0].record(stream)
+            epl.combine(cfg, y, w_d, L, out)
+            if ev is not None and dom == "combine":
+                ev[1].record(stream)
+
+    def events_for(indices):
+        return {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for i in indices}
+
+    # Timed region: K plain steps. Every 10th of them brackets only the dominant call with two
+    # HIP events (two markers per step cost about 6 us of wall time at decode, so not every step
+    # carries them). When that gives fewer than --roofline-samples launches, as at K = 20, the
+    # rest are sampled right after the timed region, on further steps of the same layer. Graph
+    # replays take no markers; the dominant call's duration then comes from the instrumented
+    # pass below.
+    in_region = events_for([i for i in range(args.steps) if i % 10 == 0] if graphs is None else [])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        if graphs is not None:
-            graphs[i % n_x].replay()
-            continue
-        ev = dev_ev.get(i)
-        if args.fused and not (ev is not None and dom == "dispatch"):
-            epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
-        else:
-            if args.fused:
-                epl.layout_counts(cfg, idx_d, out=L)
-            else:
-                epl.layout(cfg, idx_d, out=L)
-            if ev is not None:
-                ev[0].record(stream)
-            if args.fused:
-                epl.dispatch_rows(cfg, idx_d, xs[i % n_x], L, recv, recv_scale)
-            else:
-                epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
-        if ev is not None:
-            ev[1 if dom == "dispatch" else 0].record(stream)
-        epl.combine(cfg, y, w_d, L, out)
-        if ev is not None and dom == "combine":
-            ev[1].record(stream)
+    run_steps(0, args.steps, in_region)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
+    top_up = {}
+    if graphs is None and len(in_region) < args.roofline_samples:
+        n_more = args.roofline_samples - len(in_region)
+        top_up = events_for(range(args.steps, args.steps + n_more))
+        run_steps(args.steps, n_more, top_up)
+        torch.cuda.synchronize()
+    dev_ev = {**in_region, **top_up}
 
     # Per-call breakdown: a separate instrumented pass (events between every call).
     bev = timed_events(args.steps)
@@ -623,7 +641,8 @@ def main():
                 "traffic": traffic, "algorithmic_bytes": dom_bytes,
                 # the counter bytes over the same duration: the HBM rate the kernel really moved
                 "traffic_GBps": None if traffic is None else round(traffic / (dom_us * 1e-6) / 1e9, 1),
-                "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev) if dev_ev else args.steps}
+                "avg_launch_us": round(dom_us, 2), "launches_sampled": len(dev_ev) if dev_ev else args.steps,
+                "launches_sampled_in_timed_region": len(in_region) if dev_ev else 0}
 
     cpu = None
     if args.cpu_budget > 0:

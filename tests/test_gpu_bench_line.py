@@ -31,5 +31,8 @@ def test_bench_json_line():
     assert "traffic" in roof and "traffic_GBps" in roof
     assert roof["kernel"] in ("combine_kernel", "dispatch_bf16_kernel", "fused_bf16_kernel")
     cpu = d["cpu_baseline"]
-    assert cpu["kind"] == "oracle" and cpu["cores"] == 1 and cpu["value"] > 0 and cpu["sample"]
+    assert cpu["kind"] == "oracle" and cpu["cores"] >= 1 and cpu["value"] > 0 and cpu["sample"]
+    assert cpu["bit_identical_to_single_thread"] is True
+    assert cpu["single_thread"]["cores"] == 1 and cpu["single_thread"]["value"] > 0
+    assert roof["launches_sampled"] >= 20 and roof["launches_sampled_in_timed_region"] == 2
     assert d["device"]["arch"] == "gfx950"
