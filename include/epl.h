@@ -50,6 +50,8 @@ extern "C" {
 #define EPL_MAX_EXPERTS 1024 /* E (and therefore R) upper bound                        */
 #define EPL_MAX_TOPK 32      /* k upper bound                                            */
 #define EPL_MAX_HIDDEN 1048576 /* H upper bound (a row stays below 2^31 bytes)           */
+#define EPL_STATIC_SCRATCH_BYTES (8u << 20) /* workspace held by the library per GPU for
+                                               epl_layout_dispatch_noalloc                 */
 
 typedef enum {
   EPL_OK = 0,
@@ -164,6 +166,25 @@ epl_status epl_layout_counts(const epl_config *cfg, const int32_t *topk_idx, con
 epl_status epl_dispatch_rows(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
                              void *workspace, size_t workspace_bytes, const void *x, void *recv, float *recv_scale,
                              int64_t recv_rows_cap, void *stream);
+
+/* epl_layout_dispatch without a caller workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
+ * outputs, arguments, statuses and kernels as epl_layout_dispatch, except that the layout's
+ * scratch is a static device array inside the library: EPL_STATIC_SCRATCH_BYTES per GPU, held from
+ * the first call on that GPU until the process ends. The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); its first call on a GPU looks up that GPU's array.
+ * Limits and sharing:
+ *   - returns EPL_ERR_WORKSPACE, before any launch, when epl_workspace_bytes(cfg) exceeds
+ *     EPL_STATIC_SCRATCH_BYTES. 8 MiB covers every shape up to 1024 experts on 512 ranks of 64
+ *     tokens (5.1 MiB) or 256 experts on 32 ranks of 8192 tokens (3.3 MiB); 1024 ranks of one
+ *     expert each need 12 MiB and are refused;
+ *   - every call on one GPU shares that GPU's array, which keeps the last call's contents (the
+ *     kernels need no initialised scratch). Calls that overlap on one GPU (two streams, two
+ *     threads) race on it and give undefined outputs: order them on one stream;
+ *   - the array belongs to the device of `stream` (the current device for the null stream).    */
+epl_status epl_layout_dispatch_noalloc(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                                       const void *x, void *recv, float *recv_scale, int64_t recv_rows_cap,
+                                       void *stream);
 
 /* Combine: gate-weighted gather-reduce of expert output rows back into token order (the
  * paper's combine: gather expert outputs, restore token order).

@@ -2,6 +2,8 @@
 // launches on the caller's stream. Stateless and reentrant; allocates nothing.
 #include <limits.h>
 
+#include <mutex>
+
 #include "epl_internal.h"
 
 #define EPL_EXPORT extern "C" __attribute__((visibility("default")))
@@ -192,6 +194,67 @@ EPL_EXPORT epl_status epl_layout_dispatch(const epl_config* cfg, const int32_t* 
   const hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* ws = static_cast<int32_t*>(workspace);
   const hipError_t e = run_counts(g, cfg, topk_idx, L, ws, s);
+  if (e != hipSuccess) return from_hip(e);
+  return from_hip(run_rows(g, cfg, topk_idx, L, ws, x, recv, recv_scale, recv_rows_cap, s));
+}
+
+// ------------------------------------------------------------------ allocation-free variant
+// The layout workspace of epl_layout_dispatch_noalloc: one array per GPU, held by the loaded
+// library until the process ends. In host code `scratch` names a host-side stand-in, never the
+// device address; that comes from hipGetSymbolAddress, taken once per device with the device
+// current and kept in g_scratch.
+static __device__ __align__(256) int32_t scratch[EPL_STATIC_SCRATCH_BYTES / sizeof(int32_t)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int32_t* g_scratch[kMaxDevices] = {};
+
+// The device address of this GPU's scratch array (looked up on the first call for the device).
+hipError_t device_scratch(hipStream_t stream, int32_t** out) {
+  int dev = 0;
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    int cur = 0;
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+EPL_EXPORT epl_status epl_layout_dispatch_noalloc(const epl_config* cfg, const int32_t* topk_idx,
+                                                  const epl_layout_buffers* L, const void* x, void* recv,
+                                                  float* recv_scale, int64_t recv_rows_cap, void* stream) {
+  epl_status st = check_config(cfg);
+  if (st != EPL_OK) return st;
+  const epl::Geom g = make_geom(cfg);
+  if (workspace_bytes(g) > (size_t)EPL_STATIC_SCRATCH_BYTES) return EPL_ERR_WORKSPACE;
+  // The other checks are those of epl_layout_dispatch, with the static array as the workspace
+  // (a 256-byte aligned stand-in pointer passes the workspace checks; it is never dereferenced).
+  st = check_layout_dispatch(cfg, topk_idx, L, reinterpret_cast<void*>(256), (size_t)EPL_STATIC_SCRATCH_BYTES, x,
+                             recv, recv_scale, recv_rows_cap);
+  if (st != EPL_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* ws = nullptr;
+  hipError_t e = device_scratch(s, &ws);
+  if (e != hipSuccess) return from_hip(e);
+  e = run_counts(g, cfg, topk_idx, L, ws, s);
   if (e != hipSuccess) return from_hip(e);
   return from_hip(run_rows(g, cfg, topk_idx, L, ws, x, recv, recv_scale, recv_rows_cap, s));
 }

@@ -22,6 +22,7 @@ PAYLOAD_BF16 = 0
 PAYLOAD_FP8_E4M3 = 1
 MAX_EXPERTS = 1024
 MAX_TOPK = 32
+STATIC_SCRATCH_BYTES = 8 << 20  # EPL_STATIC_SCRATCH_BYTES: the library's own workspace per GPU
 
 STATUS = {0: "EPL_OK", 1: "EPL_ERR_INVALID_ARG", 2: "EPL_ERR_ALIGN", 3: "EPL_ERR_CAPACITY",
           4: "EPL_ERR_WORKSPACE", 5: "EPL_ERR_UNSUPPORTED", 6: "EPL_ERR_DEVICE"}
@@ -98,6 +99,8 @@ def lib() -> ctypes.CDLL:
         L.epl_layout_dispatch_launches.argtypes = [CP]
         L.epl_layout_launches.restype = ctypes.c_int
         L.epl_layout_launches.argtypes = [CP]
+        L.epl_layout_dispatch_noalloc.restype = ctypes.c_int
+        L.epl_layout_dispatch_noalloc.argtypes = [CP, P, LP, P, P, P, I64, P]
         _lib = L
     return _lib
 
@@ -378,6 +381,25 @@ def layout_dispatch(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: L
                                          L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
                                          sp, rows, _stream(dev)), "epl_layout_dispatch")
     return L, recv, recv_scale
+
+
+def layout_dispatch_noalloc(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: Layout,
+                            recv: torch.Tensor, recv_scale: torch.Tensor | None = None):
+    """epl_layout_dispatch_noalloc: layout and dispatch with the library's static per-GPU scratch
+    as the workspace. Every output buffer comes from the caller (out, recv, recv_scale), so nothing
+    is allocated here either; out.workspace is not used. -> (out, recv, recv_scale | None)."""
+    dev = topk_idx.device
+    _dev(topk_idx, "topk_idx", torch.int32)
+    if topk_idx.numel() != cfg.T * cfg.topk:
+        raise ValueError("topk_idx has %d elements, expected T*k = %d" % (topk_idx.numel(), cfg.T * cfg.topk))
+    _check_layout(cfg, out, dev)
+    recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
+    bufs = out.buffers()
+    with _on(dev):
+        _check(lib().epl_layout_dispatch_noalloc(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                                 x.data_ptr(), recv.data_ptr(), sp, rows, _stream(dev)),
+               "epl_layout_dispatch_noalloc")
+    return out, recv, recv_scale
 
 
 def dispatch_rows(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, L: Layout, recv: torch.Tensor | None = None,

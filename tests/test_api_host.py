@@ -181,6 +181,27 @@ def test_combine_errors(lib):
     assert cb(w=None) == INVALID
 
 
+def test_noalloc_errors_before_any_hip_call(lib):
+    """epl_layout_dispatch_noalloc reports argument errors, and a workspace beyond its static
+    scratch (1024 ranks of one expert: 12 MiB > 8 MiB), before it touches the HIP runtime."""
+    L = fake_layout()
+    idx, x, recv = Fake.ptr(50), Fake.ptr(70), Fake.ptr(71)
+    f = lambda c, idx=idx, x=x, recv=recv, sc=None, cap=1 << 20, L=L: lib.epl_layout_dispatch_noalloc(
+        ctypes.byref(c), idx, ctypes.byref(L) if L is not None else None, x, recv, sc, cap, None)
+    big = epl.config(1024, 1024, 8, 64, 16)
+    assert lib.epl_workspace_bytes(ctypes.byref(big)) > epl.STATIC_SCRATCH_BYTES
+    assert f(big, cap=1024 * 16 * 8) == WORKSPACE
+    c = cfg()
+    assert lib.epl_workspace_bytes(ctypes.byref(c)) <= epl.STATIC_SCRATCH_BYTES
+    assert f(epl.config(3, 8, 2, 64, 4)) == INVALID  # E % R != 0
+    assert f(c, cap=8 * 16 * 8 - 1) == CAPACITY
+    assert f(c, x=Fake.ptr(70, 8)) == ALIGN
+    assert f(c, idx=None) == INVALID
+    assert f(c, L=None) == INVALID
+    assert f(cfg(payload="fp8", H=7168 + 64)) == UNSUPPORTED
+    assert f(cfg(payload="fp8")) == INVALID  # no scale buffer
+
+
 def test_debug_errors(lib):
     assert lib.epl_debug_f32_to_e4m3(Fake.ptr(1), Fake.ptr(2), -1, None) == INVALID
     assert lib.epl_debug_f32_to_bf16(None, Fake.ptr(2), 5, None) == INVALID
