@@ -44,6 +44,18 @@ __device__ __forceinline__ uint32_t first_rank_mask(const int32_t* dt, int k) {
   return mask;
 }
 
+// Workgroups are dealt to the MI355X's 8 XCDs in turn (workgroup i to XCD i % 8), and each XCD
+// has its own L2. K1 and K3 take chunk xcd_chunk(i, nblk) in workgroup i, so that every XCD
+// handles one contiguous eighth of the chunks (the tail past 8 * (nblk / 8) keeps i). Their
+// small scattered stores then fall into whole lines in one L2: K1's per-chunk expert counts
+// ([E][nblk], adjacent chunks adjacent), and K3's recv_src / recv_j (within an expert, the rows
+// of adjacent chunks of a source rank are adjacent).
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_chunk(int i, int n) {
+  const int per = n / kXcds;
+  return i < per * kXcds ? (i % kXcds) * per + i / kXcds : i;
+}
+
 // ------------------------------------------------------------------------------------ K1
 __global__ void __launch_bounds__(kLayoutThreads)
     route_hist_kernel(Geom G, const int32_t* __restrict__ idx, int32_t* __restrict__ tok_nranks,
@@ -56,7 +68,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
   __shared__ int32_t red[kLayoutWaves];
 
   const int tid = threadIdx.x;
-  const int b = blockIdx.x;
+  const int b = xcd_chunk(blockIdx.x, G.nblk);
   const int s = b / G.NC;
   const int c = b - s * G.NC;
   const int t0 = c * G.CT;
@@ -350,7 +362,7 @@ __global__ void __launch_bounds__(kLayoutThreads)
   __shared__ int32_t scratch[kLayoutWaves];
 
   const int tid = threadIdx.x;
-  const int b = blockIdx.x;
+  const int b = xcd_chunk(blockIdx.x, G.nblk);
   const int s = b / G.NC;
   const int c = b - s * G.NC;
   const int t0 = c * G.CT;
