@@ -397,6 +397,14 @@ def main():
     ap.add_argument("--separate", action="store_true",
                     help="time epl_layout, epl_dispatch and epl_combine as three calls instead of "
                          "epl_layout_dispatch + epl_combine")
+    ap.add_argument("--decomposed", action="store_true",
+                    help="time epl_layout_dispatch_decomposed (layout and dispatch in one launch of count and send "
+                         "workgroups) + epl_combine")
+    ap.add_argument("--sentinel-layer", action="store_true",
+                    help="time epl_layer_sentinel: layout, dispatch and the combine of the dispatched rows in one "
+                         "launch, synchronised per row by Sentinel Polling")
+    ap.add_argument("--count-groups", type=int, default=0,
+                    help="count workgroups of the decomposed launch (0: the library's default split)")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP graph replays of the layer (one graph per x copy) instead of eager launches")
     ap.add_argument("--recv-alloc", choices=["contiguous", "torch"], default="contiguous",
@@ -490,27 +498,52 @@ def main():
     else:
         y = recv
 
-    def step(i, ev=None):
-        # Without events the default path is one epl_layout_dispatch call; with events it is
-        # issued as its two phases, so the legs are epl_layout_counts and epl_dispatch_rows.
-        if args.fused and ev is None:
-            epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
+    mode = ("sentinel" if args.sentinel_layer else "decomposed" if args.decomposed else
+            "fused" if args.fused else "separate")
+    if mode == "sentinel":
+        if w.payload != "bf16":
+            raise SystemExit("--sentinel-layer runs bf16 layers only")
+        epl.sentinel_fill(recv)  # once; every layer leaves the receive buffer so
+    status_d = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def layout_dispatch(i, mark=None):
+        """Layout and dispatch of step i. mark(), when given, runs between the layout's kernels and
+        the row kernel; the decomposed call is one launch, so there it runs before it."""
+        xi = xs[i % n_x]
+        if mode == "sentinel":  # the whole layer, combine included, in one launch
+            if mark is not None:
+                mark()
+            epl.layer_sentinel(cfg, idx_d, xi, w_d, recv, out=out, layout_out=L, count_groups=args.count_groups,
+                               status=status_d)
+        elif mode == "decomposed":
+            if mark is not None:
+                mark()
+            epl.layout_dispatch_decomposed(cfg, idx_d, xi, out=L, recv=recv, count_groups=args.count_groups,
+                                           status=status_d)
+        elif mode == "fused" and mark is None:
+            epl.layout_dispatch(cfg, idx_d, xi, out=L, recv=recv, recv_scale=recv_scale)
         else:
-            if ev is not None:
-                ev[0].record(stream)
-            if args.fused:
+            if mode == "fused":
                 epl.layout_counts(cfg, idx_d, out=L)
             else:
                 epl.layout(cfg, idx_d, out=L)
-            if ev is not None:
-                ev[1].record(stream)
-            if args.fused:
-                epl.dispatch_rows(cfg, idx_d, xs[i % n_x], L, recv, recv_scale)
+            if mark is not None:
+                mark()
+            if mode == "fused":
+                epl.dispatch_rows(cfg, idx_d, xi, L, recv, recv_scale)
             else:
-                epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
+                epl.dispatch(cfg, xi, L, recv, recv_scale)
+
+    def step(i, ev=None):
+        # With events the fused call is issued as its two phases (the same kernels), so the legs
+        # are epl_layout_counts and epl_dispatch_rows.
+        if ev is not None:
+            ev[0].record(stream)
+        layout_dispatch(i, None if ev is None else (lambda: ev[1].record(stream)))
         if ev is not None:
             ev[2].record(stream)
-        epl.combine(cfg, y, w_d, L, out)
+        if mode != "sentinel":
+            epl.combine(cfg, y, w_d, L, out)
         if ev is not None:
             ev[3].record(stream)
 
@@ -557,22 +590,15 @@ def main():
                 graphs[i % n_x].replay()
                 continue
             ev = dev_ev.get(i)
-            if args.fused and not (ev is not None and dom == "dispatch"):
-                epl.layout_dispatch(cfg, idx_d, xs[i % n_x], out=L, recv=recv, recv_scale=recv_scale)
+            if ev is not None and dom == "dispatch":
+                layout_dispatch(i, lambda: ev[0].record(stream))
+                ev[1].record(stream)
             else:
-                if args.fused:
-                    epl.layout_counts(cfg, idx_d, out=L)
-                else:
-                    epl.layout(cfg, idx_d, out=L)
+                layout_dispatch(i)
                 if ev is not None:
                     ev[0].record(stream)
-                if args.fused:
-                    epl.dispatch_rows(cfg, idx_d, xs[i % n_x], L, recv, recv_scale)
-                else:
-                    epl.dispatch(cfg, xs[i % n_x], L, recv, recv_scale)
-            if ev is not None:
-                ev[1 if dom == "dispatch" else 0].record(stream)
-            epl.combine(cfg, y, w_d, L, out)
+            if mode != "sentinel":
+                epl.combine(cfg, y, w_d, L, out)
             if ev is not None and dom == "combine":
                 ev[1].record(stream)
 
@@ -600,6 +626,15 @@ def main():
         torch.cuda.synchronize()
     dev_ev = {**in_region, **top_up}
 
+    decomposed_split = None
+    if mode == "sentinel" and int(status_d.item()) != 0:
+        raise RuntimeError("a wait of the Sentinel Polling layer gave up (status %d)" % int(status_d.item()))
+    if mode == "decomposed":
+        if int(status_d.item()) != 0:
+            raise RuntimeError("a wait of the decomposed launch gave up (status %d)" % int(status_d.item()))
+        n_count, grid, capacity = epl.decomposed_plan(cfg, args.count_groups)
+        decomposed_split = {"count": n_count, "send": grid - n_count, "capacity": capacity}
+
     # Per-call breakdown: a separate instrumented pass (events between every call).
     bev = timed_events(args.steps)
     for i in range(args.steps):
@@ -614,7 +649,8 @@ def main():
         dom_us = float(np.mean(per[:, 1 if dom == "dispatch" else 2]))
 
     pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
-    legs = ("layout_counts", "dispatch_rows") if args.fused else ("layout", "dispatch")
+    legs = {"decomposed": ("before_launch", "layout_dispatch_decomposed"), "fused": ("layout_counts", "dispatch_rows"),
+            "separate": ("layout", "dispatch"), "sentinel": ("before_launch", "layer_sentinel")}[mode]
     percentiles = {legs[0]: pct(per[:, 0]), legs[1]: pct(per[:, 1]), "combine": pct(per[:, 2]),
                    "layer": pct(per.sum(axis=1))}
 
@@ -628,11 +664,17 @@ def main():
 
     # The dispatch leg is one kernel: the plain dispatch kernel, or (epl_dispatch_rows with the
     # layout's finalize fused in) the fused row kernel, whose bytes include the placement metadata.
-    launches = epl.layout_dispatch_launches(cfg) if args.fused else None
-    row_fused = args.fused and launches == 3
-    dom_bytes = nbytes["rows_fused" if row_fused and dom == "dispatch" else dom]
+    launches = 1 if mode in ("decomposed", "sentinel") else epl.layout_dispatch_launches(cfg) if args.fused else None
+    row_fused = mode == "fused" and launches == 3
+    if mode == "decomposed" and dom == "dispatch":
+        dom_bytes = nbytes["layout"] + nbytes["dispatch"]  # the one launch does the whole layout and dispatch
+    elif mode == "sentinel":
+        dom, dom_bytes = "dispatch", nbytes["total"]  # the one launch is the whole layer
+    else:
+        dom_bytes = nbytes["rows_fused" if row_fused and dom == "dispatch" else dom]
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
-    kname = {"dispatch": "fused_bf16_kernel" if row_fused else
+    kname = {"dispatch": "decomposed_kernel" if mode in ("decomposed", "sentinel") else
+             "fused_bf16_kernel" if row_fused else
              "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
              "combine": "combine_kernel"}[dom]
     traffic = load_traffic(kname, w.name)
@@ -673,7 +715,10 @@ def main():
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2), "algorithmic_bytes_per_layer": nbytes["total"],
         "device": device_end(dinfo),
         "launch": "graph" if graphs is not None else "eager",
-        "calls": "epl_layout_dispatch + epl_combine" if args.fused else "epl_layout + epl_dispatch + epl_combine",
+        "calls": {"decomposed": "epl_layout_dispatch_decomposed + epl_combine", "sentinel": "epl_layer_sentinel",
+                  "fused": "epl_layout_dispatch + epl_combine",
+                  "separate": "epl_layout + epl_dispatch + epl_combine"}[mode],
+        "count_groups": decomposed_split,
         "layout_dispatch_launches": launches,
         "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
         "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,

@@ -167,6 +167,84 @@ epl_status epl_dispatch_rows(const epl_config *cfg, const int32_t *topk_idx, con
                              void *workspace, size_t workspace_bytes, const void *x, void *recv, float *recv_scale,
                              int64_t recv_rows_cap, void *stream);
 
+/* Options of epl_layout_dispatch_decomposed. */
+typedef struct {
+  int32_t count_groups;      /* count workgroups; 0 picks the default (one per layout chunk, at most a
+                                quarter of the workgroups the GPU holds at once); >= 0             */
+  int32_t spin_limit_us;     /* bound on every wait inside the launch, microseconds; 0 = 100000     */
+  int32_t test_ready_target; /* 0 in normal use. Tests of the give-up path set 2: the send workgroups
+                                then wait for a value no workgroup publishes, give up after
+                                spin_limit_us and store nothing, and *wait_status reports it        */
+} epl_decomposed_opts;
+
+#define EPL_WAIT_GAVE_UP_COUNT 1   /* *wait_status bit: a count workgroup stopped waiting          */
+#define EPL_WAIT_GAVE_UP_SEND 2    /* *wait_status bit: a send workgroup stopped waiting           */
+#define EPL_WAIT_GAVE_UP_COMBINE 4 /* *wait_status bit: a combine wave stopped waiting for a row   */
+#define EPL_WAIT_SENTINEL_IN_X 8   /* *wait_status bit: an input row held EPL_SENTINEL_BF16        */
+
+/* The reserved bf16 bit pattern of Sentinel Polling: a negative NaN with every payload bit set.
+ * IEEE arithmetic on the GPU returns the canonical NaN, so computed activations do not hold it;
+ * epl_sentinel_find checks a host buffer at initialisation, and the layer call reports inputs that
+ * hold it (EPL_WAIT_SENTINEL_IN_X).                                                             */
+#define EPL_SENTINEL_BF16 0xFFFFu
+
+/* Layout and dispatch in ONE launch, decomposed into count and send workgroups (Kernel
+ * Decomposition: some cores count tokens per expert and compute the CalCumSum offsets while the
+ * others send; the senders wait point to point for the published offsets instead of a global
+ * barrier). Same outputs as epl_layout_dispatch, bit for bit. Count workgroups run the layout's
+ * histogram and scans; send workgroups issue the loads of their first tokens, wait for the
+ * offsets, then place and write every row straight into its packed slot.
+ *   bf16 payloads with at most 256 pairs per layout chunk and at most 256 experts (the geometries
+ *   whose rows the send role can place per token); others return EPL_ERR_UNSUPPORTED, as does a
+ *   count_groups that leaves no room for send workgroups on the GPU.
+ *   workspace  as epl_layout_dispatch, and its last 1024 bytes (the synchronisation words) must be
+ *              zero before the first decomposed call on it: allocate it zero-filled. Every call
+ *              leaves them zero again.
+ *   wait_status [1] int32, device: written when the launch completes, 0 on success, else the
+ *              EPL_WAIT_* bits of the waits that expired; the outputs are then incomplete.
+ * The grid is sized to what the GPU holds at once, so every workgroup a wait depends on is
+ * resident; every wait is still bounded by spin_limit_us, and every workgroup runs to its end.
+ * Calls on one workspace must not overlap (order them on one stream). Other arguments and
+ * statuses as epl_layout_dispatch.                                                            */
+epl_status epl_layout_dispatch_decomposed(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                                          void *workspace, size_t workspace_bytes, const void *x, void *recv,
+                                          float *recv_scale, int64_t recv_rows_cap, const epl_decomposed_opts *opts,
+                                          int32_t *wait_status, void *stream);
+
+/* The launch shape epl_layout_dispatch_decomposed would use on the current device: returns the
+ * count workgroups (count_groups, or the default for 0) and stores the grid and the device's
+ * co-resident capacity for the kernel; -1 for a config it does not handle. Host query, no launch. */
+int epl_decomposed_plan(const epl_config *cfg, int32_t count_groups, int32_t *grid, int32_t *capacity);
+
+/* One MoE layer in ONE launch, with identity experts: layout, dispatch, and the combine of the
+ * dispatched rows (the combine reads recv itself), the combine synchronised with the dispatch per
+ * row by Sentinel Polling (Data-as-Flag; Sentinel Polling variant) instead of a kernel boundary.
+ * Count and send workgroups work as in epl_layout_dispatch_decomposed; combine workgroups wait for
+ * the offsets, work out each token's rows, and load each 16-byte piece of a row with device-scope
+ * loads until none of its elements is EPL_SENTINEL_BF16, fold it (the arithmetic of epl_combine,
+ * bit for bit), and write the sentinel back over it (the reset after consumption).
+ *   recv       [recv_rows_cap * H] bf16: every element must hold EPL_SENTINEL_BF16 before the
+ *              first call (epl_sentinel_fill); each call leaves it so. No other call may write it
+ *              in between.
+ *   x          must not hold EPL_SENTINEL_BF16 (check with epl_sentinel_find at initialisation); a
+ *              row that does is reported (EPL_WAIT_SENTINEL_IN_X) and its combine gives up.
+ *   topk_w, out  as epl_combine (out [T*H] bf16 = the combine of x's rows).
+ *   opts, wait_status  as epl_layout_dispatch_decomposed; count, send and combine waits are all
+ *              bounded by spin_limit_us.
+ * L and the workspace get the layout as epl_layout_dispatch writes it. Same shapes and statuses as
+ * epl_layout_dispatch_decomposed.                                                              */
+epl_status epl_layer_sentinel(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                              void *workspace, size_t workspace_bytes, const void *x, void *recv, int64_t recv_rows_cap,
+                              const float *topk_w, void *out, const epl_decomposed_opts *opts, int32_t *wait_status,
+                              void *stream);
+
+/* Fill kernel: n bf16 elements of buf (a multiple of 8; 16-byte aligned) set to EPL_SENTINEL_BF16. */
+epl_status epl_sentinel_fill(void *buf, int64_t n, void *stream);
+
+/* Host-only initialisation check: index of the first of n HOST bf16 values equal to
+ * EPL_SENTINEL_BF16, or -1 if none (or values is NULL or n <= 0). No HIP calls.                */
+int64_t epl_sentinel_find(const uint16_t *values, int64_t n);
+
 /* epl_layout_dispatch without a caller workspace, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
  * outputs, arguments, statuses and kernels as epl_layout_dispatch, except that the layout's

@@ -198,6 +198,88 @@ EPL_EXPORT epl_status epl_layout_dispatch(const epl_config* cfg, const int32_t* 
   return from_hip(run_rows(g, cfg, topk_idx, L, ws, x, recv, recv_scale, recv_rows_cap, s));
 }
 
+// ------------------------------------------------------------------ decomposed single launch
+namespace {
+
+epl_status decomposed_args(const epl_config* cfg, const epl_decomposed_opts* opts, epl::DecomposedOpts* out) {
+  epl::DecomposedOpts o{0, 0, 1};
+  int64_t spin_us = 100000;
+  if (opts) {
+    if (opts->count_groups < 0 || opts->spin_limit_us < 0 || opts->test_ready_target < 0) return EPL_ERR_INVALID_ARG;
+    o.count_groups = opts->count_groups;
+    if (opts->spin_limit_us > 0) spin_us = opts->spin_limit_us;
+    if (opts->test_ready_target > 0) o.ready_target = opts->test_ready_target;
+  }
+  o.spin_ticks = spin_us * 100;  // the real-time clock runs at 100 MHz
+  if (cfg->payload != EPL_PAYLOAD_BF16 || !epl::fused_dispatch_ok(make_geom(cfg), false)) return EPL_ERR_UNSUPPORTED;
+  *out = o;
+  return EPL_OK;
+}
+
+}  // namespace
+
+EPL_EXPORT epl_status epl_layout_dispatch_decomposed(const epl_config* cfg, const int32_t* topk_idx,
+                                                     const epl_layout_buffers* L, void* workspace, size_t ws_bytes,
+                                                     const void* x, void* recv, float* recv_scale,
+                                                     int64_t recv_rows_cap, const epl_decomposed_opts* opts,
+                                                     int32_t* wait_status, void* stream) {
+  epl_status st = check_layout_dispatch(cfg, topk_idx, L, workspace, ws_bytes, x, recv, recv_scale, recv_rows_cap);
+  if (st != EPL_OK) return st;
+  epl::DecomposedOpts o;
+  if ((st = decomposed_args(cfg, opts, &o)) != EPL_OK) return st;
+  if (!wait_status) return EPL_ERR_INVALID_ARG;
+  if (!aligned(wait_status, 4)) return EPL_ERR_ALIGN;
+  const epl::Geom g = make_geom(cfg);
+  epl::DecomposedPlan plan;
+  if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, false, &plan) != hipSuccess) return EPL_ERR_DEVICE;
+  if (plan.grid > plan.capacity) return EPL_ERR_UNSUPPORTED;
+  return from_hip(epl::launch_decomposed(g, topk_idx, static_cast<int32_t*>(workspace), *L, x, recv, cfg->hidden,
+                                         recv_rows_cap, o, wait_status, static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT int epl_decomposed_plan(const epl_config* cfg, int32_t count_groups, int32_t* grid, int32_t* capacity) {
+  if (check_config(cfg) != EPL_OK || count_groups < 0) return -1;
+  if (cfg->payload != EPL_PAYLOAD_BF16 || !epl::fused_dispatch_ok(make_geom(cfg), false)) return -1;
+  epl::DecomposedPlan plan;
+  if (epl::plan_decomposed(make_geom(cfg), cfg->hidden, count_groups, false, &plan) != hipSuccess) return -1;
+  if (grid) *grid = plan.grid;
+  if (capacity) *capacity = plan.capacity;
+  return plan.count_groups;
+}
+
+EPL_EXPORT epl_status epl_layer_sentinel(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                         void* workspace, size_t ws_bytes, const void* x, void* recv,
+                                         int64_t recv_rows_cap, const float* topk_w, void* out,
+                                         const epl_decomposed_opts* opts, int32_t* wait_status, void* stream) {
+  epl_status st = check_layout_dispatch(cfg, topk_idx, L, workspace, ws_bytes, x, recv, nullptr, recv_rows_cap);
+  if (st != EPL_OK) return st;
+  epl::DecomposedOpts o;
+  if ((st = decomposed_args(cfg, opts, &o)) != EPL_OK) return st;
+  const epl::Geom g = make_geom(cfg);
+  if (g.T > 0 && (!topk_w || !out)) return EPL_ERR_INVALID_ARG;
+  if (!wait_status) return EPL_ERR_INVALID_ARG;
+  if (!aligned(wait_status, 4) || !aligned(topk_w, 4) || !aligned(out, 16)) return EPL_ERR_ALIGN;
+  epl::DecomposedPlan plan;
+  if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, true, &plan) != hipSuccess) return EPL_ERR_DEVICE;
+  if (plan.grid > plan.capacity) return EPL_ERR_UNSUPPORTED;
+  return from_hip(epl::launch_decomposed(g, topk_idx, static_cast<int32_t*>(workspace), *L, x, recv, cfg->hidden,
+                                         recv_rows_cap, o, wait_status, static_cast<hipStream_t>(stream), topk_w,
+                                         out));
+}
+
+EPL_EXPORT epl_status epl_sentinel_fill(void* buf, int64_t n, void* stream) {
+  if (n < 0 || n % 8 != 0 || (n > 0 && !buf)) return EPL_ERR_INVALID_ARG;
+  if (!aligned(buf, 16)) return EPL_ERR_ALIGN;
+  return from_hip(epl::launch_sentinel_fill(buf, n / 8, static_cast<hipStream_t>(stream)));
+}
+
+EPL_EXPORT int64_t epl_sentinel_find(const uint16_t* values, int64_t n) {
+  if (!values || n <= 0) return -1;
+  for (int64_t i = 0; i < n; ++i)
+    if (values[i] == EPL_SENTINEL_BF16) return i;
+  return -1;
+}
+
 // ------------------------------------------------------------------ allocation-free variant
 // The layout workspace of epl_layout_dispatch_noalloc: one array per GPU, held by the loaded
 // library until the process ends. In host code `scratch` names a host-side stand-in, never the

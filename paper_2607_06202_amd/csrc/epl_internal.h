@@ -55,8 +55,16 @@ struct WsLayout {
   size_t inval;     // [nblk]
   size_t seg_rel;   // [E][R]     segment offsets relative to the expert start
   size_t fmask;     // [T]        per-token bitmask of first pairs per destination rank
+  size_t cnt;       // [nblk][E]  per-chunk expert counts, chunk-major (the decomposed layer's K1 rows)
+  size_t sync;      // [kSyncWords] completion words of the decomposed layer, 256-byte aligned
   size_t total;
 };
+// Words of the decomposed single-launch layer's synchronisation: zero before its first call on a
+// workspace (a zero-filled workspace), and left zero by every call. Each word the kernel polls or
+// counts on sits in a 128-byte line of its own (kSyncStride words apart): one shared line made
+// every count and poll contend.
+constexpr int kSyncStride = 32;
+constexpr int kSyncWords = 8 * kSyncStride;
 
 inline WsLayout ws_layout(const Geom& g) {
   WsLayout w;
@@ -73,6 +81,11 @@ inline WsLayout ws_layout(const Geom& g) {
   o += (size_t)g.E * g.R;
   w.fmask = o;
   o += (size_t)g.T;
+  w.cnt = o;
+  o += (size_t)g.nblk * g.E;
+  o = (o + 63) & ~(size_t)63;
+  w.sync = o;
+  o += kSyncWords;
   w.total = o;
   return w;
 }
@@ -181,6 +194,33 @@ __device__ __forceinline__ uint32_t f32x2_to_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float bf16lo_to_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
+// ---------------------------------------------------------------- cross-workgroup data
+// Loads and stores of the layout data that other workgroups of the same kernel produce or consume
+// (the decomposed single-launch layer). With C set they are device-scope accesses: sc1 loads and
+// stores, which the AMDGPU memory model uses for relaxed agent-scope atomics and which need no
+// cache write-back or invalidation; without it, plain accesses (a kernel boundary orders them).
+template <bool C>
+__device__ __forceinline__ int32_t ld32(const int32_t* p) {
+  if constexpr (C)
+    return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    return *p;
+}
+template <bool C>
+__device__ __forceinline__ uint32_t ld32(const uint32_t* p) {
+  if constexpr (C)
+    return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    return *p;
+}
+template <bool C, class T>
+__device__ __forceinline__ void st32(T* p, T v) {
+  if constexpr (C)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+
 // ---------------------------------------------------------------- launchers (host side)
 size_t single_lds_bytes(const Geom& g);
 bool layout_single(const Geom& g);  // true if epl_layout runs as one launch for this geometry
@@ -208,6 +248,29 @@ hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws,
                                  int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
                                  int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int64_t cap,
                                  hipStream_t stream);
+// The decomposed single-launch layout and dispatch (bf16, the geometries fused_dispatch_ok
+// accepts). count_groups 0 picks the default split; spin_ticks bounds every wait (100 MHz ticks);
+// ready_target is the published value the send workgroups wait for (1; a test passes 2 to force a
+// give-up). wait_status receives 0, or the give-up bits, when the launch completes.
+struct DecomposedOpts {
+  int count_groups;
+  int64_t spin_ticks;
+  int ready_target;
+};
+// Workgroups of the launch by role, and the device's co-resident capacity for it.
+struct DecomposedPlan {
+  int grid, count_groups, send_groups, combine_groups, capacity;
+};
+// layer: the variant with combine workgroups (Sentinel Polling).
+hipError_t plan_decomposed(const Geom& g, int H, int count_groups, bool layer, DecomposedPlan* plan);
+// With out != nullptr, the layer variant: combine workgroups gather the rows into out with the
+// weights topk_w as the send workgroups write them.
+hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, const epl_layout_buffers& L,
+                             const void* x, void* recv, int H, int64_t cap, const DecomposedOpts& opts,
+                             int32_t* wait_status, hipStream_t stream, const float* topk_w = nullptr,
+                             void* out = nullptr);
+// Every 16-byte vector of buf [nvec] set to the bf16 sentinel.
+hipError_t launch_sentinel_fill(void* buf, int64_t nvec, hipStream_t stream);
 hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
                           int H, hipStream_t stream);
 

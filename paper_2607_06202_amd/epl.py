@@ -53,6 +53,18 @@ def config(R: int, E: int, k: int, H: int, Tr: int, payload: str | int = "bf16")
     return Config(R, E, k, H, Tr, payload)
 
 
+class DecomposedOpts(ctypes.Structure):
+    _fields_ = [("count_groups", ctypes.c_int32), ("spin_limit_us", ctypes.c_int32),
+                ("test_ready_target", ctypes.c_int32)]
+
+
+WAIT_GAVE_UP_COUNT = 1    # EPL_WAIT_GAVE_UP_COUNT
+WAIT_GAVE_UP_SEND = 2     # EPL_WAIT_GAVE_UP_SEND
+WAIT_GAVE_UP_COMBINE = 4  # EPL_WAIT_GAVE_UP_COMBINE
+WAIT_SENTINEL_IN_X = 8    # EPL_WAIT_SENTINEL_IN_X
+SENTINEL_BF16 = 0xFFFF    # EPL_SENTINEL_BF16
+
+
 class LayoutBuffers(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("send_cnt", "rank_cnt", "expert_off", "rank_off", "seg_off",
                                                "tok_nranks", "pair_row", "pair_rslot", "recv_src", "recv_j",
@@ -99,6 +111,17 @@ def lib() -> ctypes.CDLL:
         L.epl_layout_dispatch_launches.argtypes = [CP]
         L.epl_layout_launches.restype = ctypes.c_int
         L.epl_layout_launches.argtypes = [CP]
+        L.epl_layout_dispatch_decomposed.restype = ctypes.c_int
+        L.epl_layout_dispatch_decomposed.argtypes = [CP, P, LP, P, S, P, P, P, I64, ctypes.POINTER(DecomposedOpts), P, P]
+        L.epl_decomposed_plan.restype = ctypes.c_int
+        L.epl_decomposed_plan.argtypes = [CP, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                          ctypes.POINTER(ctypes.c_int32)]
+        L.epl_layer_sentinel.restype = ctypes.c_int
+        L.epl_layer_sentinel.argtypes = [CP, P, LP, P, S, P, P, I64, P, P, ctypes.POINTER(DecomposedOpts), P, P]
+        L.epl_sentinel_fill.restype = ctypes.c_int
+        L.epl_sentinel_fill.argtypes = [P, I64, P]
+        L.epl_sentinel_find.restype = I64
+        L.epl_sentinel_find.argtypes = [P, I64]
         L.epl_layout_dispatch_noalloc.restype = ctypes.c_int
         L.epl_layout_dispatch_noalloc.argtypes = [CP, P, LP, P, P, P, I64, P]
         _lib = L
@@ -178,7 +201,7 @@ def alloc_layout(cfg: Config, device) -> Layout:
                   torch.empty(R + 1, **i32), torch.empty(E, R, **i32), torch.empty(max(T, 1), **i32),
                   torch.empty(max(T, 1), k, **i32), torch.empty(max(T, 1), k, **i32), torch.empty(max(T * k, 1), **i32),
                   torch.empty(max(T * k, 1), **i32), torch.empty(1, **i32),
-                  torch.empty(ws, dtype=torch.uint8, device=device))
+                  torch.zeros(ws, dtype=torch.uint8, device=device))  # zero: the decomposed call's sync words
 
 
 def _on(dev):
@@ -400,6 +423,94 @@ def layout_dispatch_noalloc(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor
                                                  x.data_ptr(), recv.data_ptr(), sp, rows, _stream(dev)),
                "epl_layout_dispatch_noalloc")
     return out, recv, recv_scale
+
+
+def layout_dispatch_decomposed(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, out: Layout | None = None,
+                               recv: torch.Tensor | None = None, recv_scale: torch.Tensor | None = None,
+                               count_groups: int = 0, spin_limit_us: int = 0, test_ready_target: int = 0,
+                               status: torch.Tensor | None = None):
+    """epl_layout_dispatch_decomposed: layout and dispatch in one launch of count and send
+    workgroups -> (Layout, recv, recv_scale | None, status [1] int32: 0, or EPL_WAIT_* bits, once
+    the stream reaches the end of the launch). The layout's workspace must have been allocated
+    zero-filled (alloc_layout does)."""
+    dev = topk_idx.device
+    L = _layout_args(cfg, topk_idx, out)
+    recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
+    if status is None:
+        status = torch.empty(1, dtype=torch.int32, device=dev)
+    _dev(status, "status", torch.int32)
+    _same_device(dev, status=status)
+    opts = DecomposedOpts(count_groups, spin_limit_us, test_ready_target)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_layout_dispatch_decomposed(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                                    L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(),
+                                                    recv.data_ptr(), sp, rows, ctypes.byref(opts), status.data_ptr(),
+                                                    _stream(dev)), "epl_layout_dispatch_decomposed")
+    return L, recv, recv_scale, status
+
+
+def layer_sentinel(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, topk_w: torch.Tensor, recv: torch.Tensor,
+                   out: torch.Tensor | None = None, layout_out: Layout | None = None, count_groups: int = 0,
+                   spin_limit_us: int = 0, test_ready_target: int = 0, status: torch.Tensor | None = None):
+    """epl_layer_sentinel: layout, dispatch and the combine of the dispatched rows in one launch,
+    synchronised per row by Sentinel Polling. recv must hold the sentinel everywhere (sentinel_fill)
+    and is left so. -> (Layout, out [T, H] bf16, status [1] int32)."""
+    dev = topk_idx.device
+    if cfg.payload != PAYLOAD_BF16:
+        raise EplError(5, "epl_layer_sentinel (bf16 only)")
+    L = _layout_args(cfg, topk_idx, layout_out)
+    recv, _, _, rows = _recv_args(cfg, x, recv, None, dev)
+    _dev(topk_w, "topk_w", torch.float32)
+    if _rows_of(topk_w, "topk_w", cfg.topk) < cfg.T:
+        raise ValueError("topk_w has %d rows, needs T = %d" % (topk_w.shape[0], cfg.T))
+    if out is None:
+        out = torch.empty(max(cfg.T, 1), cfg.hidden, dtype=torch.bfloat16, device=dev)
+    _dev(out, "out", torch.bfloat16)
+    if _rows_of(out, "out", cfg.hidden) < cfg.T:
+        raise ValueError("out has %d rows, needs T = %d" % (out.shape[0], cfg.T))
+    if status is None:
+        status = torch.empty(1, dtype=torch.int32, device=dev)
+    _dev(status, "status", torch.int32)
+    _same_device(dev, topk_w=topk_w, out=out, status=status)
+    opts = DecomposedOpts(count_groups, spin_limit_us, test_ready_target)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_layer_sentinel(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                        L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
+                                        rows, topk_w.data_ptr(), out.data_ptr(), ctypes.byref(opts), status.data_ptr(),
+                                        _stream(dev)), "epl_layer_sentinel")
+    return L, out, status
+
+
+def sentinel_fill(buf: torch.Tensor) -> torch.Tensor:
+    """epl_sentinel_fill over a whole contiguous bf16 GPU tensor."""
+    _dev(buf, "buf", torch.bfloat16)
+    with _on(buf.device):
+        _check(lib().epl_sentinel_fill(buf.data_ptr(), buf.numel(), _stream(buf.device)), "epl_sentinel_fill")
+    return buf
+
+
+def sentinel_find(values) -> int:
+    """epl_sentinel_find on HOST bf16 bit patterns (a numpy uint16/int16 array or a CPU bf16
+    tensor): index of the first sentinel, or -1."""
+    import numpy as np
+
+    if isinstance(values, torch.Tensor):
+        if values.device.type != "cpu":
+            raise ValueError("sentinel_find checks host memory")
+        values = values.contiguous().view(torch.int16).numpy()
+    a = np.ascontiguousarray(values).view(np.uint16)
+    return int(lib().epl_sentinel_find(a.ctypes.data_as(ctypes.c_void_p), a.size))
+
+
+def decomposed_plan(cfg: Config, count_groups: int = 0):
+    """epl_decomposed_plan on the current device -> (count workgroups, grid, co-resident capacity)."""
+    grid, cap = ctypes.c_int32(0), ctypes.c_int32(0)
+    n = lib().epl_decomposed_plan(ctypes.byref(cfg), count_groups, ctypes.byref(grid), ctypes.byref(cap))
+    if n < 0:
+        raise EplError(5, "epl_decomposed_plan(%r)" % (cfg,))
+    return n, grid.value, cap.value
 
 
 def dispatch_rows(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, L: Layout, recv: torch.Tensor | None = None,

@@ -147,7 +147,8 @@ def test_workspace_formula(lib):
         CT = min(min(want, 1024 // k), Tr) if Tr > 0 else 1
         NC = -(-Tr // CT) if Tr > 0 else 1
         nblk = R * NC
-        want_bytes = 4 * (E * nblk + nblk * R + E + nblk + E * R + T)
+        before_sync = E * nblk + nblk * R + E + nblk + E * R + T + nblk * E  # counts, totals, offsets, masks
+        want_bytes = 4 * (-(-before_sync // 64) * 64 + 256)  # then 1 KiB of synchronisation words
         assert lib.epl_workspace_bytes(ctypes.byref(epl.config(R, E, k, 64, Tr))) == want_bytes
 
 
@@ -200,6 +201,28 @@ def test_noalloc_errors_before_any_hip_call(lib):
     assert f(c, L=None) == INVALID
     assert f(cfg(payload="fp8", H=7168 + 64)) == UNSUPPORTED
     assert f(cfg(payload="fp8")) == INVALID  # no scale buffer
+
+
+def test_decomposed_errors_before_any_hip_call(lib):
+    """epl_layout_dispatch_decomposed reports bad options, unsupported payloads and shapes, and a
+    missing status word before it touches the HIP runtime."""
+    L = fake_layout()
+    idx, ws, x, recv, st = Fake.ptr(50), Fake.ptr(60), Fake.ptr(70), Fake.ptr(71), Fake.ptr(90)
+    c = epl.config(64, 256, 8, 7168, 128)
+    need = lib.epl_workspace_bytes(ctypes.byref(c))
+
+    def f(c=c, opts=None, st=st, cap=64 * 128 * 8, sc=None):
+        return lib.epl_layout_dispatch_decomposed(ctypes.byref(c), idx, ctypes.byref(L), ws, 1 << 30, x, recv, sc, cap,
+                                                  ctypes.byref(opts) if opts is not None else None, st, None)
+    assert f(opts=epl.DecomposedOpts(-1, 0, 0)) == INVALID
+    assert f(opts=epl.DecomposedOpts(0, -5, 0)) == INVALID
+    assert f(opts=epl.DecomposedOpts(0, 0, -1)) == INVALID
+    assert f(c=epl.config(64, 256, 8, 7168, 128, "fp8"), sc=Fake.ptr(72)) == UNSUPPORTED
+    assert f(c=epl.config(64, 512, 8, 7168, 128)) == UNSUPPORTED          # 512 experts
+    assert f(c=epl.config(64, 256, 8, 7168, 130), cap=64 * 130 * 8) == UNSUPPORTED  # 264 pairs per chunk
+    assert f(st=None) == INVALID
+    assert f(st=Fake.ptr(90, 2)) == ALIGN
+    assert f(cap=64 * 128 * 8 - 1) == CAPACITY
 
 
 def test_debug_errors(lib):
@@ -258,3 +281,39 @@ def test_contiguous_block_views_must_fit_the_block():
         b.tensor((51,), torch.bfloat16)  # 102 bytes
     with pytest.raises(ValueError):
         b.tensor((3, 34), torch.uint8)  # 102 bytes
+
+
+def test_sentinel_find_on_the_host(lib):
+    """The initialisation check for Sentinel Polling runs on the host: the first index of the
+    reserved bf16 pattern, or -1; other NaNs, infinities and every other pattern pass."""
+    import numpy as np
+
+    assert epl.SENTINEL_BF16 == 0xFFFF
+    every = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    assert epl.sentinel_find(every) == 0xFFFF
+    others = every[every != 0xFFFF]
+    assert epl.sentinel_find(others) == -1
+    x = W.normal_bf16(3, W.STREAM_X, 4096)
+    assert epl.sentinel_find(x) == -1
+    x[1234] = 0xFFFF
+    x[3000] = 0xFFFF
+    assert epl.sentinel_find(x) == 1234
+    assert lib.epl_sentinel_find(None, 5) == -1
+    assert epl.sentinel_find(np.zeros(0, np.uint16)) == -1
+
+
+def test_layer_sentinel_errors_before_any_hip_call(lib):
+    L = fake_layout()
+    c = epl.config(4, 16, 2, 256, 128)
+    idx, ws, x, recv, w, out, st = (Fake.ptr(i) for i in (50, 60, 70, 71, 80, 81, 90))
+
+    def f(c=c, w=w, out=out, st=st, opts=None):
+        return lib.epl_layer_sentinel(ctypes.byref(c), idx, ctypes.byref(L), ws, 1 << 30, x, recv, 4 * 128 * 2, w, out,
+                                      ctypes.byref(opts) if opts is not None else None, st, None)
+    assert f(w=None) == INVALID
+    assert f(out=Fake.ptr(81, 8)) == ALIGN
+    assert f(st=None) == INVALID
+    assert f(opts=epl.DecomposedOpts(-1, 0, 0)) == INVALID
+    assert f(c=epl.config(4, 16, 2, 256, 128, "fp8")) == INVALID  # fp8 needs a scale buffer first
+    assert lib.epl_sentinel_fill(Fake.ptr(1), 12, None) == INVALID  # not a multiple of 8 elements
+    assert lib.epl_sentinel_fill(Fake.ptr(1, 8), 16, None) == ALIGN
