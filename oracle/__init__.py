@@ -51,6 +51,8 @@ def lib() -> ctypes.CDLL:
             "eplref_combine": (None, [L, I, I, P, P, P, P, L, P]),
             "eplref_combine_mapped": (None, [I, I, P, P, P, P, P, L, P]),
             "eplref_locate_rows": (None, [I, P, L, P, P, P]),
+            "eplref_transposed_order": (None, [I, I, P]),
+            "eplref_hop_schedule": (None, [I, I, I, I, P, P, P, P, P, P]),
             "eplref_f32_to_bf16_array": (None, [P, P, L]),
             "eplref_f32_to_e4m3_array": (None, [P, P, L]),
             "eplref_f32_to_bf16": (ctypes.c_uint16, [ctypes.c_float]),
@@ -219,6 +221,31 @@ def locate_rows(expert_off: np.ndarray, rows=None, n: int | None = None):
     offset = np.empty(n, np.int32)
     lib().eplref_locate_rows(E, _p(off), n, None if rows is None else _p(rows), _p(expert), _p(offset))
     return expert, offset
+
+
+def transposed_order(E: int, rows: int) -> np.ndarray:
+    """The remapped expert sequence of the logical matrix transposition: E experts laid row by row
+    in a matrix of ``rows`` rows (the paper: one per worker), read column by column (Hierarchical
+    Token-level Scheduling, Expert Remapping via Logical Matrix Transposition)."""
+    order = np.zeros(E, np.int32)
+    lib().eplref_transposed_order(E, rows, _p(order))
+    return order
+
+
+def hop_schedule(send_cnt: np.ndarray, order: np.ndarray, hop: np.ndarray, n: int, NH: int):
+    """Equal slices of each source rank's pairs, taken in the expert sequence ``order``, for n workers
+    -> (start_expert [R, n], start_offset [R, n], counts [R, n, NH]): each slice's first expert and
+    offset, and its pairs per hop class hop[s, d] of their destination rank d (Token-level Load
+    Partition; the per-hop counts v_{j,h} of Latency Homogenization)."""
+    send_cnt = np.ascontiguousarray(send_cnt, np.int32)
+    R, E = send_cnt.shape
+    order = np.ascontiguousarray(order, np.int32)
+    hop = np.ascontiguousarray(hop, np.int32).reshape(R, R)
+    se = np.zeros((R, n), np.int32)
+    so = np.zeros((R, n), np.int32)
+    cnt = np.zeros((R, n, NH), np.int32)
+    lib().eplref_hop_schedule(R, E, n, NH, _p(send_cnt), _p(order), _p(hop), _p(se), _p(so), _p(cnt))
+    return se, so, cnt
 
 
 def f32_to_bf16(v: np.ndarray) -> np.ndarray:

@@ -343,3 +343,65 @@ REF_API void eplref_locate_rows(int E, const int32_t *expert_off, int64_t n, con
       }
   }
 }
+
+/* ------------------------------------------------------------------------------------------
+ * Hierarchical token-level scheduling (Hierarchical Token-level Scheduling: latency
+ * homogenization, the hardware-accelerated mapper's expert remapping by logical matrix
+ * transposition and token-level load partition).
+ *
+ * The remapped expert sequence, as the reading of the transposition: a virtual matrix of `rows`
+ * rows (the paper: one row per worker) and c = ceil(E/rows) columns holds the experts in their
+ * natural order, row by row (row w holds experts w*c .. w*c+c-1, the block a worker would take
+ * without the remap); the sequence reads it column by column, skipping the cells past E.
+ * ------------------------------------------------------------------------------------------ */
+REF_API void eplref_transposed_order(int E, int rows, int32_t *order) {
+  const int c = (E + rows - 1) / rows;
+  int i = 0;
+  for (int col = 0; col < c; ++col)
+    for (int row = 0; row < rows; ++row) {
+      const int e = row * c + col;
+      if (e < E) order[i++] = e;
+    }
+}
+
+/* For each source rank s: the pairs it sends, taken expert by expert in the sequence `order`
+ * (order[i] is the i-th expert; it contributes send_cnt[s][order[i]] pairs), are cut into n
+ * contiguous slices whose sizes differ by at most one: slice j is positions
+ * [floor(j*m/n), floor((j+1)*m/n)) of the m pairs. Worker j of source s gets
+ *   start_expert[s*n+j], start_offset[s*n+j]: the expert of the slice's first position and that
+ *       position's offset among the expert's pairs (-1, -1 for an empty slice);
+ *   counts[(s*n+j)*NH+h]: the slice's pairs whose destination rank d = e / (E/R) has hop class
+ *       hop[s*R+d] == h, for 0 <= h < NH (a class outside that range is counted nowhere).
+ * Written as the plain definition: the overlap of every expert's range with the slice. */
+REF_API void eplref_hop_schedule(int R, int E, int n, int NH, const int32_t *send_cnt, const int32_t *order,
+                                 const int32_t *hop, int32_t *start_expert, int32_t *start_offset,
+                                 int32_t *counts) {
+  const int El = E / R;
+  for (int s = 0; s < R; ++s) {
+    int64_t m = 0;
+    for (int e = 0; e < E; ++e) m += send_cnt[(int64_t)s * E + e];
+    for (int j = 0; j < n; ++j) {
+      const int64_t lo = (int64_t)j * m / n, hi = (int64_t)(j + 1) * m / n;
+      int32_t *cnt = counts + ((int64_t)s * n + j) * NH;
+      for (int h = 0; h < NH; ++h) cnt[h] = 0;
+      start_expert[(int64_t)s * n + j] = -1;
+      start_offset[(int64_t)s * n + j] = -1;
+      int64_t base = 0;
+      for (int i = 0; i < E; ++i) {
+        const int e = order[i];
+        const int64_t c = send_cnt[(int64_t)s * E + e];
+        const int64_t a = base > lo ? base : lo;
+        const int64_t b = base + c < hi ? base + c : hi;
+        if (b > a) {
+          const int32_t h = hop[(int64_t)s * R + e / El];
+          if (h >= 0 && h < NH) cnt[h] += (int32_t)(b - a);
+          if (start_expert[(int64_t)s * n + j] < 0) {
+            start_expert[(int64_t)s * n + j] = e;
+            start_offset[(int64_t)s * n + j] = (int32_t)(lo - base);
+          }
+        }
+        base += c;
+      }
+    }
+  }
+}
