@@ -403,6 +403,11 @@ def main():
     ap.add_argument("--sentinel-layer", action="store_true",
                     help="time epl_layer_sentinel: layout, dispatch and the combine of the dispatched rows in one "
                          "launch, synchronised per row by Sentinel Polling")
+    ap.add_argument("--scheduled", type=int, default=0, metavar="WORKERS",
+                    help="time epl_layout + epl_dispatch_scheduled (WORKERS workgroups per source rank, each "
+                         "sending one equal slice of the rank's pairs in the transposed expert order) + epl_combine")
+    ap.add_argument("--remap-rows", type=int, default=0,
+                    help="rows of the expert transposition of --scheduled (0: one per worker; 1: natural order)")
     ap.add_argument("--count-groups", type=int, default=0,
                     help="count workgroups of the decomposed launch (0: the library's default split)")
     ap.add_argument("--graph", action="store_true",
@@ -499,7 +504,9 @@ def main():
         y = recv
 
     mode = ("sentinel" if args.sentinel_layer else "decomposed" if args.decomposed else
-            "fused" if args.fused else "separate")
+            "scheduled" if args.scheduled else "fused" if args.fused else "separate")
+    if mode == "scheduled" and w.payload != "bf16":
+        raise SystemExit("--scheduled runs bf16 layers only")
     if mode == "sentinel":
         if w.payload != "bf16":
             raise SystemExit("--sentinel-layer runs bf16 layers only")
@@ -520,6 +527,11 @@ def main():
                 mark()
             epl.layout_dispatch_decomposed(cfg, idx_d, xi, out=L, recv=recv, count_groups=args.count_groups,
                                            status=status_d)
+        elif mode == "scheduled":
+            epl.layout(cfg, idx_d, out=L)
+            if mark is not None:
+                mark()
+            epl.dispatch_scheduled(cfg, xi, L, args.scheduled, remap_rows=args.remap_rows, recv=recv)
         elif mode == "fused" and mark is None:
             epl.layout_dispatch(cfg, idx_d, xi, out=L, recv=recv, recv_scale=recv_scale)
         else:
@@ -650,7 +662,8 @@ def main():
 
     pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
     legs = {"decomposed": ("before_launch", "layout_dispatch_decomposed"), "fused": ("layout_counts", "dispatch_rows"),
-            "separate": ("layout", "dispatch"), "sentinel": ("before_launch", "layer_sentinel")}[mode]
+            "separate": ("layout", "dispatch"), "sentinel": ("before_launch", "layer_sentinel"),
+            "scheduled": ("layout", "dispatch_scheduled")}[mode]
     percentiles = {legs[0]: pct(per[:, 0]), legs[1]: pct(per[:, 1]), "combine": pct(per[:, 2]),
                    "layer": pct(per.sum(axis=1))}
 
@@ -664,7 +677,7 @@ def main():
 
     # The dispatch leg is one kernel: the plain dispatch kernel, or (epl_dispatch_rows with the
     # layout's finalize fused in) the fused row kernel, whose bytes include the placement metadata.
-    launches = 1 if mode in ("decomposed", "sentinel") else epl.layout_dispatch_launches(cfg) if args.fused else None
+    launches = 1 if mode in ("decomposed", "sentinel") else epl.layout_dispatch_launches(cfg) if mode == "fused" else None
     row_fused = mode == "fused" and launches == 3
     if mode == "decomposed" and dom == "dispatch":
         dom_bytes = nbytes["layout"] + nbytes["dispatch"]  # the one launch does the whole layout and dispatch
@@ -674,6 +687,7 @@ def main():
         dom_bytes = nbytes["rows_fused" if row_fused and dom == "dispatch" else dom]
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
     kname = {"dispatch": "decomposed_kernel" if mode in ("decomposed", "sentinel") else
+             "dispatch_scheduled_kernel" if mode == "scheduled" else
              "fused_bf16_kernel" if row_fused else
              "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
              "combine": "combine_kernel"}[dom]
@@ -717,8 +731,11 @@ def main():
         "launch": "graph" if graphs is not None else "eager",
         "calls": {"decomposed": "epl_layout_dispatch_decomposed + epl_combine", "sentinel": "epl_layer_sentinel",
                   "fused": "epl_layout_dispatch + epl_combine",
-                  "separate": "epl_layout + epl_dispatch + epl_combine"}[mode],
+                  "separate": "epl_layout + epl_dispatch + epl_combine",
+                  "scheduled": "epl_layout + epl_dispatch_scheduled + epl_combine"}[mode],
         "count_groups": decomposed_split,
+        "schedule": {"workers": args.scheduled, "remap_rows": args.remap_rows or args.scheduled}
+        if mode == "scheduled" else None,
         "layout_dispatch_launches": launches,
         "per_call_us_p10_p50_p90": percentiles, "layout_launches": epl.layout_launches(cfg),
         "fabric_equivalent_bytes": fabric_pairs * row_bytes, "fabric_row_pairs": fabric_pairs,

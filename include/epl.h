@@ -292,6 +292,49 @@ epl_status epl_combine(const epl_config *cfg, const void *y, const float *topk_w
 epl_status epl_locate_rows(const epl_config *cfg, const int32_t *expert_off, const int32_t *rows, int64_t n,
                            int32_t *expert, int32_t *offset, void *stream);
 
+#define EPL_MAX_HOP_CLASSES 8 /* hop classes of epl_hop_schedule                             */
+
+/* Hierarchical token-level schedule (Hierarchical Token-level Scheduling: Latency Homogenization;
+ * Hardware-Accelerated Mapper, Expert Remapping via Logical Matrix Transposition and Token-level
+ * Load Partition). For every source rank s, its valid pairs are taken expert by expert in a
+ * remapped expert sequence (expert order[i] contributes send_cnt[s*E+order[i]] pairs) and cut into
+ * `workers` contiguous slices whose sizes differ by at most one: worker j gets positions
+ * [floor(j*m/n), floor((j+1)*m/n)) of the rank's m pairs, n = workers. For each (s, j):
+ *   start_expert[s*n+j], start_offset[s*n+j]  the expert holding the slice's first position and
+ *              that position's offset among the expert's pairs (Algorithm 1's lookup over the
+ *              remapped cumulative counts); -1, -1 for an empty slice;
+ *   class_cnt[(s*n+j)*NH+h]  the slice's pairs whose destination rank d = e / (E/R) has hop class
+ *              hop_class[s*R+d] == h, 0 <= h < NH = num_classes (the per-hop loads v_{j,h}; the
+ *              remap aims for v_{j,h} <= ceil(V_h / n)). A class outside [0, NH) is counted nowhere.
+ * The sequence:
+ *   order      [E] int32 device, the expert sequence, or NULL for the transposition: the experts
+ *              laid row by row into a matrix of remap_rows rows and ceil(E/remap_rows) columns
+ *              (row w holds the block of experts worker w would take without the remap), read
+ *              column by column, skipping empty cells. remap_rows 0 means one row per worker
+ *              (remap_rows = workers); remap_rows 1 gives the natural order 0..E-1. An order entry
+ *              outside [0, E) counts as an expert with no pairs.
+ *   send_cnt   [R*E] int32 device, a layout's send_cnt (or any non-negative counts).
+ *   hop_class  [R*R] int32 device, hop class of each (source, destination rank).
+ * workers >= 1 and R*workers < 2^31; 1 <= num_classes <= EPL_MAX_HOP_CLASSES; remap_rows >= 0
+ * (INVALID_ARG otherwise); pointers 4-byte aligned (ALIGN). One launch of R workgroups.        */
+epl_status epl_hop_schedule(const epl_config *cfg, const int32_t *send_cnt, const int32_t *order, int32_t remap_rows,
+                            const int32_t *hop_class, int32_t workers, int32_t num_classes, int32_t *start_expert,
+                            int32_t *start_offset, int32_t *class_cnt, void *stream);
+
+/* Dispatch in the order of the hierarchical token-level schedule: one workgroup per (source rank
+ * s, worker j) sends slice j of s's pairs, taken in the transposed expert sequence of
+ * epl_hop_schedule (order NULL, same remap_rows and workers), each pair's row copied from x into
+ * its packed receive row. Every worker moves floor(m/n) or ceil(m/n) rows. The output is the same
+ * as epl_dispatch's, bit for bit: only which workgroup writes a row, and when, follows the
+ * schedule. Each pair reads its token's row of x (k reads per token where epl_dispatch reads it
+ * once), as per-pair sends do.
+ *   bf16 payloads only (EPL_ERR_UNSUPPORTED otherwise).
+ *   L          a layout of the same cfg: send_cnt, seg_off and recv_src are read.
+ *   x, recv, recv_rows_cap  as epl_dispatch.
+ * workers >= 1 and R*workers < 2^31, remap_rows >= 0, else INVALID_ARG.                        */
+epl_status epl_dispatch_scheduled(const epl_config *cfg, const void *x, const epl_layout_buffers *L, void *recv,
+                                  int64_t recv_rows_cap, int32_t remap_rows, int32_t workers, void *stream);
+
 /* Diagnostics: apply the exact device number conversions used by epl_dispatch (fp32 ->
  * saturating E4M3) and epl_combine (fp32 -> bf16 RNE) to n values, for exhaustive checks.
  * in [n] fp32, out [n] bytes / bf16 bit patterns, 4-byte aligned; n >= 0.                   */

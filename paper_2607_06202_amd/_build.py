@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libepl.so")
-SOURCES = ["api.hip", "layout.hip", "dispatch.hip", "decomposed.hip", "combine.hip", "locate.hip"]
+SOURCES = ["api.hip", "layout.hip", "dispatch.hip", "decomposed.hip", "combine.hip", "locate.hip", "schedule.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

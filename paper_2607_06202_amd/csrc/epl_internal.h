@@ -152,6 +152,34 @@ __device__ __forceinline__ int block_exclusive_sum(int v, int& total, int* scrat
   return pre + inc - v;
 }
 
+// ---------------------------------------------------------------- quaternary search
+// Position lookup over a non-decreasing list of cumulative counts off[0..n] with off[0] = 0
+// (Algorithm 1, Quaternary Search, with the loop ending once the window holds one entry): for
+// 0 <= t < off[n], the index i with off[i] <= t < off[i + 1], i.e. the non-empty entry whose
+// cumulative range covers t. The window [L, R) keeps off[L] <= t < off[R]; a step reads the counts
+// at three cut points as independent loads and keeps the quarter that holds t, so it ends after
+// ceil(log4 n) steps. off may live in LDS or global memory.
+__device__ __forceinline__ int quaternary_find(const int32_t* off, int n, int64_t t) {
+  int L = 0, R = n;
+  while (R - L > 1) {
+    const int gap = (R - L + 3) >> 2;
+    const int p1 = min(L + gap, R), p2 = min(L + 2 * gap, R), p3 = min(L + 3 * gap, R);
+    const int c1 = off[p1], c2 = off[p2], c3 = off[p3];
+    if (t < c1) {
+      R = p1;
+    } else if (t < c2) {
+      L = p1;
+      R = p2;
+    } else if (t < c3) {
+      L = p2;
+      R = p3;
+    } else {
+      L = p3;
+    }
+  }
+  return L;
+}
+
 // ---------------------------------------------------------------- number conversions
 // Clamp to [-448, 448], letting NaN through: the median of three returns -448 for a NaN.
 __device__ __forceinline__ float clamp_e4m3(float v) {
@@ -276,6 +304,12 @@ hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row
 
 hipError_t launch_locate_rows(const int32_t* expert_off, const int32_t* rows, int64_t n, int E, int32_t* expert,
                               int32_t* offset, hipStream_t stream);
+hipError_t launch_hop_schedule(const int32_t* send_cnt, const int32_t* order, const int32_t* hop, int R, int E,
+                               int rows, int n, int NH, int32_t* start_expert, int32_t* start_offset,
+                               int32_t* class_cnt, hipStream_t stream);
+hipError_t launch_dispatch_scheduled(const void* x, const int32_t* send_cnt, const int32_t* seg_off,
+                                     const int32_t* recv_src, void* recv, int R, int E, int rows, int n, int64_t T,
+                                     int k, int H, int64_t cap, hipStream_t stream);
 hipError_t launch_debug_e4m3(const float* in, uint8_t* out, int64_t n, hipStream_t stream);
 hipError_t launch_debug_bf16(const float* in, uint16_t* out, int64_t n, hipStream_t stream);
 

@@ -28,27 +28,8 @@ __global__ void __launch_bounds__(kLocateThreads)
     const int64_t t = rows ? (int64_t)rows[q] : q;
     int e = -1, o = -1;
     if (t >= 0 && t < P) {
-      // Window [L, R) of experts with off[L] <= t < off[R]. Every step leaves at most
-      // ceil((R - L) / 4) experts, so it ends with one: the non-empty expert that holds t.
-      int L = 0, R = E;
-      while (R - L > 1) {
-        const int gap = (R - L + 3) >> 2;
-        const int p1 = min(L + gap, R), p2 = min(L + 2 * gap, R), p3 = min(L + 3 * gap, R);
-        const int c1 = off[p1], c2 = off[p2], c3 = off[p3];
-        if (t < c1) {
-          R = p1;
-        } else if (t < c2) {
-          L = p1;
-          R = p2;
-        } else if (t < c3) {
-          L = p2;
-          R = p3;
-        } else {
-          L = p3;
-        }
-      }
-      e = L;
-      o = (int)(t - off[L]);
+      e = quaternary_find(off, E, t);
+      o = (int)(t - off[e]);
     }
     expert[q] = e;
     offset[q] = o;

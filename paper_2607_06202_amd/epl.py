@@ -22,6 +22,7 @@ PAYLOAD_BF16 = 0
 PAYLOAD_FP8_E4M3 = 1
 MAX_EXPERTS = 1024
 MAX_TOPK = 32
+MAX_HOP_CLASSES = 8  # EPL_MAX_HOP_CLASSES
 STATIC_SCRATCH_BYTES = 8 << 20  # EPL_STATIC_SCRATCH_BYTES: the library's own workspace per GPU
 
 STATUS = {0: "EPL_OK", 1: "EPL_ERR_INVALID_ARG", 2: "EPL_ERR_ALIGN", 3: "EPL_ERR_CAPACITY",
@@ -124,6 +125,11 @@ def lib() -> ctypes.CDLL:
         L.epl_sentinel_find.argtypes = [P, I64]
         L.epl_layout_dispatch_noalloc.restype = ctypes.c_int
         L.epl_layout_dispatch_noalloc.argtypes = [CP, P, LP, P, P, P, I64, P]
+        I32 = ctypes.c_int32
+        L.epl_hop_schedule.restype = ctypes.c_int
+        L.epl_hop_schedule.argtypes = [CP, P, P, I32, P, I32, I32, P, P, P, P]
+        L.epl_dispatch_scheduled.restype = ctypes.c_int
+        L.epl_dispatch_scheduled.argtypes = [CP, P, LP, P, I64, I32, I32, P]
         _lib = L
     return _lib
 
@@ -547,6 +553,51 @@ def locate_rows(cfg: Config, L: Layout, rows: torch.Tensor | None = None, n: int
                                      None if rows is None else rows.data_ptr(), n, expert.data_ptr(),
                                      offset.data_ptr(), _stream(dev)), "epl_locate_rows")
     return expert[:n], offset[:n]
+
+
+def hop_schedule(cfg: Config, send_cnt: torch.Tensor, hop_class: torch.Tensor, workers: int, num_classes: int,
+                 remap_rows: int = 0, order: torch.Tensor | None = None):
+    """epl_hop_schedule: send_cnt [R, E] and hop_class [R, R] int32 on the GPU (order [E] int32, or
+    None for the transposition with remap_rows rows, 0 = one per worker) -> (start_expert [R, n],
+    start_offset [R, n], class_cnt [R, n, num_classes]) int32, n = workers."""
+    dev = send_cnt.device
+    R, E = cfg.num_ranks, cfg.num_experts
+    _dev(send_cnt, "send_cnt", torch.int32)
+    _dev(hop_class, "hop_class", torch.int32)
+    if send_cnt.numel() != R * E or hop_class.numel() != R * R:
+        raise ValueError("send_cnt must hold R*E and hop_class R*R values")
+    if order is not None:
+        _dev(order, "order", torch.int32)
+        if order.numel() != E:
+            raise ValueError("order must hold E values")
+    _same_device(dev, hop_class=hop_class, order=order)
+    i32 = dict(dtype=torch.int32, device=dev)
+    n = max(int(workers), 1)
+    se = torch.empty(R, n, **i32)
+    so = torch.empty(R, n, **i32)
+    cnt = torch.empty(R, n, max(int(num_classes), 1), **i32)
+    with _on(dev):
+        _check(lib().epl_hop_schedule(ctypes.byref(cfg), send_cnt.data_ptr(),
+                                      None if order is None else order.data_ptr(), remap_rows,
+                                      hop_class.data_ptr(), workers, num_classes, se.data_ptr(), so.data_ptr(),
+                                      cnt.data_ptr(), _stream(dev)), "epl_hop_schedule")
+    return se, so, cnt
+
+
+def dispatch_scheduled(cfg: Config, x: torch.Tensor, L: Layout, workers: int, remap_rows: int = 0,
+                       recv: torch.Tensor | None = None) -> torch.Tensor:
+    """epl_dispatch_scheduled: the rows of epl_dispatch, written by one workgroup per (source rank,
+    worker) in the order of the hierarchical token-level schedule -> recv [cap, H] bf16."""
+    dev = x.device
+    if cfg.payload != PAYLOAD_BF16:
+        raise EplError(5, "epl_dispatch_scheduled (bf16 only)")
+    _check_layout(cfg, L, dev)
+    recv, _, _, rows = _recv_args(cfg, x, recv, None, dev)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_dispatch_scheduled(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(),
+                                            rows, remap_rows, workers, _stream(dev)), "epl_dispatch_scheduled")
+    return recv
 
 
 def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):

@@ -332,3 +332,11 @@ def device_normal_bf16(shape, seed: int, device):
     g = torch.Generator(device=device)
     g.manual_seed(int(seed))
     return torch.randn(*shape, generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+
+
+def node_hop_classes(R: int, ranks_per_node: int = 8) -> np.ndarray:
+    """Hop class of every (source rank, destination rank) for R ranks placed ranks_per_node to a node
+    (8 GPUs on one xGMI node): 0 within the source's node, 1 across nodes -> [R, R] int32. A topology
+    input of the hierarchical schedule, not part of its arithmetic."""
+    node = np.arange(R) // ranks_per_node
+    return (node[:, None] != node[None, :]).astype(np.int32)

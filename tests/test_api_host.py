@@ -317,3 +317,40 @@ def test_layer_sentinel_errors_before_any_hip_call(lib):
     assert f(c=epl.config(4, 16, 2, 256, 128, "fp8")) == INVALID  # fp8 needs a scale buffer first
     assert lib.epl_sentinel_fill(Fake.ptr(1), 12, None) == INVALID  # not a multiple of 8 elements
     assert lib.epl_sentinel_fill(Fake.ptr(1, 8), 16, None) == ALIGN
+
+
+def test_schedule_errors_before_any_hip_call(lib):
+    """epl_hop_schedule and epl_dispatch_scheduled report bad worker counts, class counts, remap
+    rows, payloads, missing buffers, misalignment and capacity before they touch the HIP runtime."""
+    c = epl.config(64, 256, 8, 7168, 128)
+    sc, hop, se, so, cc = Fake.ptr(10), Fake.ptr(11), Fake.ptr(12), Fake.ptr(13), Fake.ptr(14)
+
+    def hs(c=c, sc=sc, order=None, rows=0, hop=hop, n=32, nh=2, se=se, so=so, cc=cc):
+        return lib.epl_hop_schedule(ctypes.byref(c), sc, order, rows, hop, n, nh, se, so, cc, None)
+    assert hs(n=0) == INVALID
+    assert hs(n=1 << 30) == INVALID          # R * workers >= 2^31
+    assert hs(nh=0) == INVALID
+    assert hs(nh=epl.MAX_HOP_CLASSES + 1) == INVALID
+    assert hs(rows=-1) == INVALID
+    assert hs(sc=None) == INVALID
+    assert hs(hop=None) == INVALID
+    assert hs(cc=None) == INVALID
+    assert hs(order=Fake.ptr(15, 2)) == ALIGN
+    assert hs(se=Fake.ptr(12, 1)) == ALIGN
+    assert hs(c=epl.config(3, 16, 8, 64, 4)) == INVALID  # E % R != 0
+
+    L = fake_layout()
+    x, recv = Fake.ptr(70), Fake.ptr(71)
+
+    def ds(c=c, x=x, recv=recv, cap=64 * 128 * 8, rows=0, n=32, L=L):
+        return lib.epl_dispatch_scheduled(ctypes.byref(c), x, ctypes.byref(L) if L is not None else None, recv, cap,
+                                          rows, n, None)
+    assert ds(c=epl.config(64, 256, 8, 7168, 128, "fp8")) == UNSUPPORTED
+    assert ds(n=0) == INVALID
+    assert ds(rows=-2) == INVALID
+    assert ds(L=None) == INVALID
+    assert ds(L=fake_layout(null_field="seg_off")) == INVALID
+    assert ds(L=fake_layout(null_field="recv_src")) == INVALID
+    assert ds(x=None) == INVALID
+    assert ds(x=Fake.ptr(70, 8)) == ALIGN
+    assert ds(cap=64 * 128 * 8 - 1) == CAPACITY
