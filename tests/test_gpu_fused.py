@@ -58,6 +58,9 @@ def _check(R, E, k, Tr, H, payload, seed, idx=None, phases=False):
     (64, 256, 8, 100, 8, 5, 3),      # 200 pairs per chunk; one 16-byte vector per row
     (16, 64, 8, 1024, 64, 6, 4),     # 512 pairs per chunk
     (8, 1024, 32, 1024, 64, 7, 4),   # k = 32, E = 1024
+    (256, 256, 8, 64, 1032, 11, 4),  # the EP=256 chunking: 512 pairs per chunk, ragged last column chunk
+    (4, 1024, 32, 300, 1032, 12, 4), # 1024 pairs per chunk, 1024 experts, ragged chunks
+    (1024, 1024, 2, 40, 64, 13, 4),  # 1024 ranks of one expert
     (64, 256, 8, 40, 4096, 8, 3),    # 2 column chunks per row: 2 tokens per workgroup
     (32, 256, 8, 130, 6152, 9, 3),   # 4 chunks, the last one ragged (769 vectors per row)
     (64, 256, 8, 40, 10240, 10, 3),  # 5 chunks: a workgroup's waves straddle two tokens
