@@ -1,6 +1,7 @@
 // Standalone C++ consumer of the C ABI in include/epl.h: no Python, no torch. It allocates
-// device buffers with the HIP runtime, runs layout -> dispatch -> combine and the row location on
-// its own stream, and compares every output with the CPU oracle (oracle/liboracle.so, test
+// device buffers with the HIP runtime, runs layout -> dispatch -> combine, the row location, the
+// hierarchical schedule and the dispatch in its order on its own stream, and compares every output
+// with the CPU oracle (oracle/liboracle.so, test
 // infrastructure), then checks that host-detectable errors are reported before anything is launched.
 // Prints "c abi check ok" and exits 0 on success; prints the first difference and exits 1.
 #include <hip/hip_runtime_api.h>
@@ -25,6 +26,9 @@ void eplref_combine(int64_t T, int k, int H, const uint16_t* y, const float* w, 
                     const int64_t* tokens, int64_t n_tokens, uint16_t* out);
 void eplref_locate_rows(int E, const int32_t* expert_off, int64_t n, const int32_t* rows, int32_t* expert,
                         int32_t* offset);
+void eplref_transposed_order(int E, int rows, int32_t* order);
+void eplref_hop_schedule(int R, int E, int n, int NH, const int32_t* send_cnt, const int32_t* order,
+                         const int32_t* hop, int32_t* start_expert, int32_t* start_offset, int32_t* counts);
 }
 
 #define HIP_OK(x)                                                                              \
@@ -176,6 +180,43 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
     ok = ok && same("locate expert", host_copy(d_le, n), le, n) && same("locate offset", host_copy(d_lo, n), lo, n);
     HIP_OK(hipFree(d_le));
     HIP_OK(hipFree(d_lo));
+  }
+
+  if (ok && !fp8 && T > 0) {  // the hierarchical schedule and the dispatch in its order
+    const int n = 6, NH = 2;
+    std::vector<int32_t> hop((size_t)c.R * c.R), order(c.E);
+    for (int a = 0; a < c.R; ++a)
+      for (int b = 0; b < c.R; ++b) hop[(size_t)a * c.R + b] = (a / 8 == b / 8) ? 0 : 1;  // nodes of 8 ranks
+    eplref_transposed_order(c.E, n, order.data());
+    std::vector<int32_t> se((size_t)c.R * n), so((size_t)c.R * n), cnt((size_t)c.R * n * NH);
+    eplref_hop_schedule(c.R, c.E, n, NH, r_send.data(), order.data(), hop.data(), se.data(), so.data(), cnt.data());
+    int32_t* d_hop = dev_copy(hop);
+    int32_t *d_se = nullptr, *d_so = nullptr, *d_cnt = nullptr;
+    HIP_OK(hipMalloc(&d_se, se.size() * 4));
+    HIP_OK(hipMalloc(&d_so, so.size() * 4));
+    HIP_OK(hipMalloc(&d_cnt, cnt.size() * 4));
+    void* d_recv2 = nullptr;
+    HIP_OK(hipMalloc(&d_recv2, std::max<size_t>(1, (size_t)Tk * c.H * 2)));
+    ok = epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, n, NH, d_se, d_so, d_cnt, stream) == EPL_OK &&
+         epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, Tk, 0, n, stream) == EPL_OK;
+    HIP_OK(hipStreamSynchronize(stream));
+    std::vector<uint16_t> rr((size_t)Tk * c.H);
+    eplref_dispatch_bf16(T, c.k, c.H, x.data(), r_row.data(), rr.data());
+    ok = ok && same("schedule start expert", host_copy(d_se, se.size()), se, se.size()) &&
+         same("schedule start offset", host_copy(d_so, so.size()), so, so.size()) &&
+         same("schedule class counts", host_copy(d_cnt, cnt.size()), cnt, cnt.size()) &&
+         same("scheduled dispatch rows", host_copy((const uint16_t*)d_recv2, (size_t)P * c.H), rr, (size_t)P * c.H);
+    ok = ok && epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, 0, NH, d_se, d_so, d_cnt, stream) ==
+                   EPL_ERR_INVALID_ARG &&
+         epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, n, EPL_MAX_HOP_CLASSES + 1, d_se, d_so, d_cnt, stream) ==
+             EPL_ERR_INVALID_ARG &&
+         epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, Tk - 1, 0, n, stream) == EPL_ERR_CAPACITY &&
+         epl_dispatch_scheduled(&cfg, (char*)d_x + 2, &L, d_recv2, Tk, 0, n, stream) == EPL_ERR_ALIGN;
+    HIP_OK(hipFree(d_hop));
+    HIP_OK(hipFree(d_se));
+    HIP_OK(hipFree(d_so));
+    HIP_OK(hipFree(d_cnt));
+    HIP_OK(hipFree(d_recv2));
   }
 
   // Host-detectable errors come back before any launch.
