@@ -18,6 +18,7 @@
 //   order of the writes and the split of the work across workgroups follow the schedule. Each pair
 //   reads its token's row again, as the paper's per-pair sends do (k reads of a token instead of
 //   one).
+#include "layout_body.h"
 #include "rows_body.h"
 
 namespace epl {
@@ -143,7 +144,7 @@ __global__ void __launch_bounds__(kScheduleThreads)
   }
 }
 
-// One workgroup per (source rank s, worker j), j fastest. The slice's positions are handled in
+// One workgroup per (source rank s, worker j). The slice's positions are handled in
 // batches of one per thread: each thread locates its position (Algorithm 1's lookup over the
 // remapped cumulative counts), takes the pair's packed row seg_off[e][s] + offset and its token
 // recv_src[row], and shares both through LDS; the waves then copy the batch's rows, one
@@ -160,8 +161,11 @@ __global__ void __launch_bounds__(kScheduleThreads)
   __shared__ int32_t row_lds[kScheduleThreads];
   __shared__ int32_t src_lds[kScheduleThreads];
   __shared__ int scratch[kLayoutWaves];
-  const int s = blockIdx.x / n;
-  const int j = blockIdx.x - s * n;
+  // Workgroup i runs on XCD i % 8; xcd_chunk gives each XCD a contiguous range of (source, worker)
+  // slices, so a source's workers share one L2 for the token rows they all read.
+  const int u = xcd_chunk((int)blockIdx.x, (int)gridDim.x);
+  const int s = u / n;
+  const int j = u - s * n;
   const int lane = threadIdx.x % kWave;
   const int64_t Tk = T * k;
   remapped_counts(send_cnt + (int64_t)s * E, nullptr, E, rows, exp_at, cnt_at, cum, scratch);
