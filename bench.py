@@ -271,8 +271,8 @@ def cpu_baseline(w, idx, x, gw, budget_s, threads):
     """The oracle, unchanged, timed on this host's CPU on the same inputs, two ways:
     * single thread: oracle.layout, then the dispatch and the combine over all tokens;
     * `threads` threads: the same layout call, then the unchanged dispatch and combine functions
-      called on disjoint token ranges from a thread pool (ctypes releases the GIL), the
-      partition the survey's multi-thread mode names for scatter and combine.
+      called on disjoint token ranges from a thread pool (ctypes releases the GIL): scatter and
+      combine split by token range, the layout kept serial.
     The threaded layer's receive rows and output must equal the single-thread ones bit for bit.
     For fp8 the combine reads a bf16 buffer of zeros, as the GPU layer does. Each leg runs whole
     layers until its half of the budget is spent (at least one)."""
