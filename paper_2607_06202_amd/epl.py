@@ -622,6 +622,79 @@ def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: 
     return out
 
 
+class PreparedLayer:
+    """One MoE layer's calls with every argument checked and converted once, for loops that issue
+    the same layer many times (a serving loop, a benchmark). layout_dispatch(i) is
+    epl_layout_dispatch with x = xs[i % len(xs)], layout_counts() and dispatch_rows(i) are its two
+    phases, combine() is epl_combine, and run(i) is layout_dispatch(i) then combine(); each is one
+    C call with prebuilt arguments on the stream current at construction. Construction makes the
+    checks the plain calls make; afterwards the tensors must stay alive and keep their shapes, and
+    the calls must be made with the same current device."""
+
+    def __init__(self, cfg: Config, topk_idx: torch.Tensor, xs, topk_w: torch.Tensor, L: Layout,
+                 recv: torch.Tensor, recv_scale: torch.Tensor | None = None, y: torch.Tensor | None = None,
+                 out: torch.Tensor | None = None):
+        dev = topk_idx.device
+        xs = list(xs)
+        if not xs:
+            raise ValueError("give at least one x")
+        L = _layout_args(cfg, topk_idx, L)
+        sp = rows = None
+        for x in xs:
+            recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
+        y = recv if y is None else y
+        _dev(y, "y", torch.bfloat16)
+        _rows_of(y, "y", cfg.hidden)
+        _dev(topk_w, "topk_w", torch.float32)
+        if _rows_of(topk_w, "topk_w", cfg.topk) < cfg.T:
+            raise ValueError("topk_w has %d rows, needs T = %d" % (topk_w.shape[0], cfg.T))
+        if out is None:
+            out = torch.empty(max(cfg.T, 1), cfg.hidden, dtype=torch.bfloat16, device=dev)
+        _dev(out, "out", torch.bfloat16)
+        if _rows_of(out, "out", cfg.hidden) < cfg.T:
+            raise ValueError("out has %d rows, needs T = %d" % (out.shape[0], cfg.T))
+        _same_device(dev, y=y, topk_w=topk_w, out=out)
+        if torch.cuda.current_device() != dev.index:
+            raise ValueError("make %s the current device before preparing its layer" % dev)
+        self.cfg, self.L, self.recv, self.recv_scale, self.y, self.out = cfg, L, recv, recv_scale, y, out
+        self._keep = (topk_idx, xs, topk_w)
+        bufs = L.buffers()
+        self._bufs = bufs
+        cp, bp, st = ctypes.byref(cfg), ctypes.byref(bufs), _stream(dev)
+        ws, wsn = L.workspace.data_ptr(), L.workspace.numel()
+        lb = lib()
+        self._ld, self._lc, self._dr, self._cb = (lb.epl_layout_dispatch, lb.epl_layout_counts, lb.epl_dispatch_rows,
+                                                  lb.epl_combine)
+        self._ld_args = [(cp, topk_idx.data_ptr(), bp, ws, wsn, x.data_ptr(), recv.data_ptr(), sp, rows, st)
+                         for x in xs]
+        self._lc_args = (cp, topk_idx.data_ptr(), bp, ws, wsn, st)
+        self._cb_args = (cp, y.data_ptr(), topk_w.data_ptr(), bp, out.data_ptr(), st)
+
+    def layout_dispatch(self, i: int = 0) -> None:
+        s = self._ld(*self._ld_args[i % len(self._ld_args)])
+        if s:
+            raise EplError(s, "epl_layout_dispatch")
+
+    def layout_counts(self) -> None:
+        s = self._lc(*self._lc_args)
+        if s:
+            raise EplError(s, "epl_layout_counts")
+
+    def dispatch_rows(self, i: int = 0) -> None:
+        s = self._dr(*self._ld_args[i % len(self._ld_args)])
+        if s:
+            raise EplError(s, "epl_dispatch_rows")
+
+    def combine(self) -> None:
+        s = self._cb(*self._cb_args)
+        if s:
+            raise EplError(s, "epl_combine")
+
+    def run(self, i: int = 0) -> None:
+        self.layout_dispatch(i)
+        self.combine()
+
+
 def debug_f32_to_e4m3(v: torch.Tensor) -> torch.Tensor:
     _dev(v, "v", torch.float32)
     out = torch.empty(v.numel(), dtype=torch.uint8, device=v.device)

@@ -239,6 +239,13 @@ def test_binding_rejects_host_tensors_before_any_call():
         epl.layout(cfg_, torch.zeros(6, 2, dtype=torch.int32))
     with pytest.raises(ValueError):
         epl.debug_f32_to_e4m3(torch.zeros(4))
+    L = epl.Layout(cfg_, *[torch.zeros(1, dtype=torch.int32)] * 11, torch.zeros(1, dtype=torch.uint8))
+    with pytest.raises(ValueError):
+        epl.PreparedLayer(cfg_, torch.zeros(6, 2, dtype=torch.int32), [torch.zeros(6, 64, dtype=torch.bfloat16)],
+                          torch.zeros(6, 2), L, torch.zeros(12, 64, dtype=torch.bfloat16))
+    with pytest.raises(ValueError):
+        epl.PreparedLayer(cfg_, torch.zeros(6, 2, dtype=torch.int32), [], torch.zeros(6, 2), L,
+                          torch.zeros(12, 64, dtype=torch.bfloat16))
 
 
 from hypothesis import given, settings, strategies as st  # noqa: E402

@@ -14,7 +14,7 @@ import torch
 import oracle
 from paper_2607_06202_amd import epl
 from paper_2607_06202_amd import workloads as W
-from tests.gpu_util import assert_layout_equal, bf16_bits, device, to_dev_bf16
+from tests.gpu_util import LAYOUT_FIELDS, assert_layout_equal, bf16_bits, device, to_dev_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -171,3 +171,46 @@ def test_fused_row_kernel_with_buffer_loads():
         src = torch.from_numpy(ref.recv_src.astype(np.int64)).to(dev)
         assert torch.equal(recv[:ref.P].view(torch.int16), x_d[src].view(torch.int16))
         del L, recv
+
+
+@pytest.mark.parametrize("R,E,k,Tr,H,seed,payload", [
+    (64, 256, 8, 40, 1024, 20, "bf16"),   # finalize fused into the row kernel
+    (4, 16, 2, 128, 256, 21, "bf16"),     # one-launch layout
+    (16, 64, 8, 300, 1032, 22, "bf16"),   # three-launch layout, then the plain dispatch
+    (16, 64, 8, 40, 1152, 23, "fp8"),     # fp8: three-launch layout, then the fp8 dispatch
+])
+def test_prepared_layer_matches_the_plain_calls(R, E, k, Tr, H, seed, payload):
+    """PreparedLayer (arguments checked and converted once) issues the same calls as
+    epl_layout_dispatch + epl_combine: identical layout, rows and output, for every x it rotates
+    through, both as run(i) and as the two phases plus combine."""
+    dev = device()
+    T = R * Tr
+    cfg = epl.config(R, E, k, H, Tr, payload)
+    idx = W.with_replacement(seed, T, k, -1, E + 1).astype(np.int32)
+    idx_d = torch.from_numpy(idx).to(dev)
+    xs = [to_dev_bf16(W.normal_bf16(seed + i, W.STREAM_X, T * H).reshape(T, H), dev) for i in range(2)]
+    w_d = torch.from_numpy(W.softmax_gate_weights(seed, T, k)).to(dev)
+    fp8 = payload == "fp8"
+    y = torch.from_numpy(W.normal_bf16(seed, W.STREAM_Y, T * k * H).reshape(T * k, H).view(np.int16)).view(
+        torch.bfloat16).to(dev) if fp8 else None
+    L = epl.alloc_layout(cfg, dev)
+    recv, scale = epl.alloc_recv(cfg, dev)
+    prep = epl.PreparedLayer(cfg, idx_d, xs, w_d, L, recv, scale, y=y)
+    for i, x in enumerate(xs):
+        L2, r2, s2 = epl.layout_dispatch(cfg, idx_d, x)
+        o2 = epl.combine(cfg, r2 if not fp8 else y, w_d, L2)
+        for phases in (False, True):
+            if phases:
+                prep.layout_counts()
+                prep.dispatch_rows(i)
+                prep.combine()
+            else:
+                prep.run(i)
+            torch.cuda.synchronize()
+            P = int(L2.expert_off[-1].item())
+            for name in LAYOUT_FIELDS:
+                assert torch.equal(getattr(prep.L, name), getattr(L2, name)), (name, i, phases)
+            assert torch.equal(prep.recv[:P].view(torch.uint8), r2[:P].view(torch.uint8)), (i, phases)
+            if fp8:
+                assert torch.equal(prep.recv_scale[:P].view(torch.int32), s2[:P].view(torch.int32)), (i, phases)
+            assert torch.equal(prep.out[:T].view(torch.int16), o2[:T].view(torch.int16)), (i, phases)
