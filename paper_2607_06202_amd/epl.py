@@ -656,11 +656,14 @@ class PreparedLayer:
         _same_device(dev, y=y, topk_w=topk_w, out=out)
         if torch.cuda.current_device() != dev.index:
             raise ValueError("make %s the current device before preparing its layer" % dev)
-        self.cfg, self.L, self.recv, self.recv_scale, self.y, self.out = cfg, L, recv, recv_scale, y, out
-        self._keep = (topk_idx, xs, topk_w)
-        bufs = L.buffers()
-        self._bufs = bufs
-        cp, bp, st = ctypes.byref(cfg), ctypes.byref(bufs), _stream(dev)
+        self.L, self.recv, self.recv_scale, self.y, self.out = L, recv, recv_scale, y, out
+        # A private copy of the config and of the pointer struct, and a reference to every tensor
+        # whose address is baked into the calls: changing the caller's cfg, or replacing a field
+        # of L, later leaves these calls as they were checked.
+        self.cfg = Config(*[getattr(cfg, f) for f, _ in Config._fields_])
+        self._bufs = LayoutBuffers(*[getattr(L, n).data_ptr() for n, _ in LayoutBuffers._fields_])
+        self._keep = (topk_idx, xs, topk_w, [getattr(L, n) for n, _ in LayoutBuffers._fields_], L.workspace)
+        cp, bp, st = ctypes.byref(self.cfg), ctypes.byref(self._bufs), _stream(dev)
         ws, wsn = L.workspace.data_ptr(), L.workspace.numel()
         lb = lib()
         self._ld, self._lc, self._dr, self._cb = (lb.epl_layout_dispatch, lb.epl_layout_counts, lb.epl_dispatch_rows,
