@@ -163,9 +163,9 @@ __global__ void __launch_bounds__(kScheduleThreads)
   __shared__ int scratch[kLayoutWaves];
   // Workgroup i runs on XCD i % 8; xcd_chunk gives each XCD a contiguous range of (source, worker)
   // slices, so a source's workers share one L2 for the token rows they all read.
-  const int u = xcd_chunk((int)blockIdx.x, (int)gridDim.x);
-  const int s = u / n;
-  const int j = u - s * n;
+  const int slice = xcd_chunk((int)blockIdx.x, (int)gridDim.x);
+  const int s = slice / n;
+  const int j = slice - s * n;
   const int lane = threadIdx.x % kWave;
   const int64_t Tk = T * k;
   remapped_counts(send_cnt + (int64_t)s * E, nullptr, E, rows, exp_at, cnt_at, cum, scratch);
