@@ -78,15 +78,17 @@ def test_schedule_matches_oracle_explicit_order(seed):
 
 @pytest.mark.parametrize("name", ["decode_ep64", "skewed_fp8_ep64", "large_ep256", "prefill_ep32"])
 @pytest.mark.parametrize("n", [32, 48])
-def test_schedule_on_the_named_layouts(name, n):
-    """The counts of each named workload's own layout, 8-rank nodes as the two hop classes."""
+@pytest.mark.parametrize("rows_per", ["worker", "node"])
+def test_schedule_on_the_named_layouts(name, n, rows_per):
+    """The counts of each named workload's own layout, 8-rank nodes as the two hop classes, the
+    transposition with one matrix row per worker or one per node."""
     dev = device()
     w = W.WORKLOADS[name]
     idx = W.routing(w)
     _, L = run_layout(w, idx, dev)
     send = L.send_cnt.cpu().numpy()
     hop = W.node_hop_classes(w.R)
-    got, want = _schedule_both(send, hop, n, 2)
+    got, want = _schedule_both(send, hop, n, 2, rows=0 if rows_per == "worker" else w.R // 8)
     _assert_same(got, want, name)
     # every slice holds floor(m/n) or ceil(m/n) pairs, and the classes add up to the rank's pairs
     sizes = got[2].sum(axis=2)
