@@ -196,3 +196,28 @@ def test_small_exhaustive_orders():
             want = _brute_schedule(send, order, hop, n, NH)
             for g, w in zip(got, want):
                 np.testing.assert_array_equal(g, w)
+
+
+def test_transposition_evens_out_the_hop_mix_of_the_decode_layout():
+    """The decode workload's own counts (64 ranks in 8 nodes of 8, 256 experts, 32 workers): the
+    variance of each hop class's load across workers, summed over the classes (tr of the covariance,
+    the paper's objective), falls under the transposition, and most with one matrix row per node,
+    where every slice draws experts from all nodes."""
+    from paper_2607_06202_amd import workloads as W
+
+    w = W.WORKLOADS["decode_ep64"]
+    ref = oracle.layout(w.R, w.E, w.k, w.Tr, W.routing(w))
+    send = ref.send_cnt.reshape(w.R, w.E)
+    hop = W.node_hop_classes(w.R)
+    n = 32
+
+    def tr_sigma(order):
+        _, _, cnt = oracle.hop_schedule(send, order, hop, n, 2)
+        np.testing.assert_array_equal(cnt.sum(axis=(1, 2)), send.sum(axis=1))  # every pair counted once
+        return cnt.astype(np.float64).var(axis=1).sum(axis=1).mean()
+
+    natural = tr_sigma(np.arange(w.E, dtype=np.int32))
+    per_worker = tr_sigma(oracle.transposed_order(w.E, n))
+    per_node = tr_sigma(oracle.transposed_order(w.E, w.R // 8))
+    assert per_node < per_worker < natural
+    assert natural > 10 * per_node
