@@ -18,7 +18,7 @@ import torch
 import oracle
 from paper_2607_06202_amd import epl
 from paper_2607_06202_amd import workloads as W
-from tests.gpu_util import assert_layout_equal, bf16_bits, bf16_ulp_distance, device, run_layout, to_dev_bf16
+from tests.gpu_util import assert_layout_equal, bf16_bits, bf16_ulp_distance, device, to_dev_bf16
 
 pytestmark = pytest.mark.gpu
 
