@@ -280,11 +280,26 @@ _HIP_DEVICE_MALLOC_CONTIGUOUS = 0x4  # hipDeviceMallocContiguous
 _hip = None
 
 
+def _hip_runtime_path() -> str:
+    """The HIP runtime this process already has mapped (torch's and libepl's), else its soname."""
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                path = line.split()[-1] if line.strip() else ""
+                if os.path.basename(path).startswith("libamdhip64.so"):
+                    return path
+    except OSError:
+        pass
+    return "libamdhip64.so.7"
+
+
 def _hip_runtime() -> ctypes.CDLL:
-    """The HIP runtime that torch and libepl already share (same soname, so no second copy)."""
+    """The HIP runtime that torch and libepl already share: the mapped file itself when it is found
+    in the process's memory map (so no second copy is loaded), else by soname."""
     global _hip
     if _hip is None:
-        h = ctypes.CDLL("libamdhip64.so.7")
+        lib()  # libepl links the runtime, so it is mapped from here on
+        h = ctypes.CDLL(_hip_runtime_path())
         h.hipExtMallocWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t, ctypes.c_uint]
         h.hipExtMallocWithFlags.restype = ctypes.c_int
         h.hipFree.argtypes = [ctypes.c_void_p]
