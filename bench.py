@@ -505,8 +505,6 @@ def main():
 
     mode = ("sentinel" if args.sentinel_layer else "decomposed" if args.decomposed else
             "scheduled" if args.scheduled else "fused" if args.fused else "separate")
-    if mode == "scheduled" and w.payload != "bf16":
-        raise SystemExit("--scheduled runs bf16 layers only")
     if mode == "sentinel":
         if w.payload != "bf16":
             raise SystemExit("--sentinel-layer runs bf16 layers only")
@@ -531,7 +529,8 @@ def main():
             epl.layout(cfg, idx_d, out=L)
             if mark is not None:
                 mark()
-            epl.dispatch_scheduled(cfg, xi, L, args.scheduled, remap_rows=args.remap_rows, recv=recv)
+            epl.dispatch_scheduled(cfg, xi, L, args.scheduled, remap_rows=args.remap_rows, recv=recv,
+                                   recv_scale=recv_scale)
         elif mode == "fused" and mark is None:
             epl.layout_dispatch(cfg, idx_d, xi, out=L, recv=recv, recv_scale=recv_scale)
         else:

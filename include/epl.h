@@ -327,13 +327,14 @@ epl_status epl_hop_schedule(const epl_config *cfg, const int32_t *send_cnt, cons
  * its packed receive row. Every worker moves floor(m/n) or ceil(m/n) rows. The output is the same
  * as epl_dispatch's, bit for bit: only which workgroup writes a row, and when, follows the
  * schedule. Each pair reads its token's row of x (k reads per token where epl_dispatch reads it
- * once), as per-pair sends do.
- *   bf16 payloads only (EPL_ERR_UNSUPPORTED otherwise).
+ * once), as per-pair sends do; fp8 payloads are quantised per pair, with epl_dispatch's rule.
  *   L          a layout of the same cfg: send_cnt, seg_off and recv_src are read.
- *   x, recv, recv_rows_cap  as epl_dispatch.
- * workers >= 1 and R*workers < 2^31, remap_rows >= 0, else INVALID_ARG.                        */
+ *   x, recv, recv_scale, recv_rows_cap  as epl_dispatch (recv_scale fp8 only, else ignored).
+ * workers >= 1 and R*workers < 2^31, remap_rows >= 0, else INVALID_ARG; other statuses as
+ * epl_dispatch.                                                                                 */
 epl_status epl_dispatch_scheduled(const epl_config *cfg, const void *x, const epl_layout_buffers *L, void *recv,
-                                  int64_t recv_rows_cap, int32_t remap_rows, int32_t workers, void *stream);
+                                  float *recv_scale, int64_t recv_rows_cap, int32_t remap_rows, int32_t workers,
+                                  void *stream);
 
 /* Diagnostics: apply the exact device number conversions used by epl_dispatch (fp32 ->
  * saturating E4M3) and epl_combine (fp32 -> bf16 RNE) to n values, for exhaustive checks.

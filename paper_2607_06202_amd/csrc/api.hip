@@ -378,23 +378,24 @@ EPL_EXPORT epl_status epl_hop_schedule(const epl_config* cfg, const int32_t* sen
 }
 
 EPL_EXPORT epl_status epl_dispatch_scheduled(const epl_config* cfg, const void* x, const epl_layout_buffers* L,
-                                             void* recv, int64_t recv_rows_cap, int32_t remap_rows, int32_t workers,
-                                             void* stream) {
+                                             void* recv, float* recv_scale, int64_t recv_rows_cap, int32_t remap_rows,
+                                             int32_t workers, void* stream) {
   const epl_status st = check_config(cfg);
   if (st != EPL_OK) return st;
-  if (cfg->payload != EPL_PAYLOAD_BF16) return EPL_ERR_UNSUPPORTED;
+  const bool fp8 = cfg->payload == EPL_PAYLOAD_FP8_E4M3;
+  if (fp8 && cfg->hidden % 128 != 0) return EPL_ERR_UNSUPPORTED;
   if (workers < 1 || (int64_t)cfg->num_ranks * workers >= (int64_t)INT_MAX || remap_rows < 0)
     return EPL_ERR_INVALID_ARG;
   if (!L || !L->send_cnt || !L->seg_off || !L->recv_src) return EPL_ERR_INVALID_ARG;
   if (!aligned(L->send_cnt, 4) || !aligned(L->seg_off, 4) || !aligned(L->recv_src, 4)) return EPL_ERR_ALIGN;
   const int64_t T = (int64_t)cfg->num_ranks * cfg->tokens_per_rank;
-  if (T > 0 && (!x || !recv)) return EPL_ERR_INVALID_ARG;
-  if (!aligned(x, 16) || !aligned(recv, 16)) return EPL_ERR_ALIGN;
+  if (T > 0 && (!x || !recv || (fp8 && !recv_scale))) return EPL_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(recv, 16) || (fp8 && !aligned(recv_scale, 4))) return EPL_ERR_ALIGN;
   if (recv_rows_cap < T * cfg->topk) return EPL_ERR_CAPACITY;
-  return from_hip(epl::launch_dispatch_scheduled(x, L->send_cnt, L->seg_off, L->recv_src, recv, cfg->num_ranks,
-                                                 cfg->num_experts, remap_rows ? remap_rows : workers, workers, T,
-                                                 cfg->topk, cfg->hidden, recv_rows_cap,
-                                                 static_cast<hipStream_t>(stream)));
+  return from_hip(epl::launch_dispatch_scheduled(x, L->send_cnt, L->seg_off, L->recv_src, recv,
+                                                 fp8 ? recv_scale : nullptr, cfg->num_ranks, cfg->num_experts,
+                                                 remap_rows ? remap_rows : workers, workers, T, cfg->topk,
+                                                 cfg->hidden, recv_rows_cap, static_cast<hipStream_t>(stream)));
 }
 
 EPL_EXPORT epl_status epl_combine(const epl_config* cfg, const void* y, const float* topk_w,

@@ -42,54 +42,6 @@ __global__ void __launch_bounds__(kPlainThreads)
   }
 }
 
-// fp8: unit = (token g, pass p) covering elements [1024p, 1024p + 1024). Lane l quantises
-// elements [16l, 16l+16) of the pass: two 16-byte bf16 loads -> one 16-byte E4M3 store per
-// destination. A 128-element block spans 8 lanes, whose max is combined with three
-// xor-shuffles; the first lane of each block stores that block's scale for every destination.
-template <class RowFn>
-__device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
-                                                  float* __restrict__ recv_scale, int64_t g, int p, int k, int H,
-                                                  int64_t cap, int lane) {
-  const int NB = H / 128;
-  const int nvq = H / 16;  // 16-byte fp8 vectors per row
-  const u32x4* xr = x + g * (H / 8);
-  const int vq = p * kWave + lane;  // fp8 vector index = element / 16
-  const bool on = vq < nvq;         // whole 8-lane blocks are on or off (H % 128 == 0)
-  const int vl = min(vq, nvq - 1);  // clamped so the loads need no branch
-  u32x4 a = xr[2 * vl];
-  u32x4 bv = xr[2 * vl + 1];
-  const int my_row = row_of();
-  if (!on) a = bv = u32x4{0, 0, 0, 0};
-  float f[16];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f[2 * i] = bf16lo_to_f32(a[i]);
-    f[2 * i + 1] = bf16hi_to_f32(a[i]);
-    f[8 + 2 * i] = bf16lo_to_f32(bv[i]);
-    f[8 + 2 * i + 1] = bf16hi_to_f32(bv[i]);
-  }
-  float amax = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(f[i]));
-  amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
-  amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
-  amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
-  const float s = amax / 448.0f;
-  u32x4 q = {0, 0, 0, 0};
-  if (amax != 0.0f) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      q[i] = f32x4_to_e4m3x4(f[4 * i] / s, f[4 * i + 1] / s, f[4 * i + 2] / s, f[4 * i + 3] / s);
-  }
-  const bool scale_lane = on && (lane % 8) == 0;
-  for (int j = 0; j < k; ++j) {
-    const int row = __builtin_amdgcn_readlane(my_row, j);
-    if (row < 0 || row >= cap) continue;
-    if (on) store_row_policy<kCachePolicySc1Nt>(q, recv + (int64_t)row * nvq, nvq, vq);
-    if (scale_lane) recv_scale[(int64_t)row * NB + vq / 8] = s;
-  }
-}
-
 // The fp8 kernel is capped at kFp8WavesPerSimd waves per SIMD. The compiler enforces the cap by
 // reserving a larger register budget. Each wave writes up to k scattered 1 KiB q rows per 2 KiB of
 // input, so fewer resident waves keep fewer concurrent random writes in flight; too few leave the

@@ -307,9 +307,10 @@ hipError_t launch_locate_rows(const int32_t* expert_off, const int32_t* rows, in
 hipError_t launch_hop_schedule(const int32_t* send_cnt, const int32_t* order, const int32_t* hop, int R, int E,
                                int rows, int n, int NH, int32_t* start_expert, int32_t* start_offset,
                                int32_t* class_cnt, hipStream_t stream);
+// recv_scale non-null: fp8 payload (rows quantised as in launch_dispatch_fp8).
 hipError_t launch_dispatch_scheduled(const void* x, const int32_t* send_cnt, const int32_t* seg_off,
-                                     const int32_t* recv_src, void* recv, int R, int E, int rows, int n, int64_t T,
-                                     int k, int H, int64_t cap, hipStream_t stream);
+                                     const int32_t* recv_src, void* recv, float* recv_scale, int R, int E, int rows,
+                                     int n, int64_t T, int k, int H, int64_t cap, hipStream_t stream);
 hipError_t launch_debug_e4m3(const float* in, uint8_t* out, int64_t n, hipStream_t stream);
 hipError_t launch_debug_bf16(const float* in, uint16_t* out, int64_t n, hipStream_t stream);
 

@@ -14,10 +14,10 @@
 //   first expert and offset (Algorithm 1's lookup) and its pairs per hop class;
 // * dispatch_scheduled_kernel, one workgroup per (source rank, worker): the worker's slice of
 //   pairs, taken in the remapped order, each copied from its token's row of x into its packed
-//   receive row. The rows are those of the layout, so the output equals epl_dispatch's; only the
-//   order of the writes and the split of the work across workgroups follow the schedule. Each pair
-//   reads its token's row again, as the paper's per-pair sends do (k reads of a token instead of
-//   one).
+//   receive row (quantised to fp8 on the way for fp8 payloads). The rows are those of the layout, so
+//   the output equals epl_dispatch's; only the order of the writes and the split of the work across
+//   workgroups follow the schedule. Each pair reads its token's row again, as the paper's per-pair
+//   sends do (k reads of a token instead of one).
 #include "layout_body.h"
 #include "rows_body.h"
 
@@ -149,12 +149,14 @@ __global__ void __launch_bounds__(kScheduleThreads)
 // remapped cumulative counts), takes the pair's packed row seg_off[e][s] + offset and its token
 // recv_src[row], and shares both through LDS; the waves then copy the batch's rows, one
 // (row, 4 KiB column chunk) unit per wave as the token-major dispatch does, with one destination.
-template <bool BUF_X>
+// FP8: each row is quantised as it is copied, by the fp8 dispatch's unit (token, 1024-element pass)
+// with one destination; units per row is then the number of passes.
+template <bool BUF_X, bool FP8>
 __global__ void __launch_bounds__(kScheduleThreads)
     dispatch_scheduled_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ send_cnt,
                               const int32_t* __restrict__ seg_off, const int32_t* __restrict__ recv_src,
-                              u32x4* __restrict__ recv, int R, int E, int rows, int n, int64_t T, int k, int nv,
-                              int chunks, int64_t cap) {
+                              u32x4* __restrict__ recv, float* __restrict__ recv_scale, int R, int E, int rows, int n,
+                              int64_t T, int k, int H, int chunks, int64_t cap) {
   __shared__ int32_t exp_at[EPL_MAX_EXPERTS];
   __shared__ int32_t cnt_at[EPL_MAX_EXPERTS];
   __shared__ int32_t cum[EPL_MAX_EXPERTS + 1];
@@ -189,7 +191,10 @@ __global__ void __launch_bounds__(kScheduleThreads)
       const int row = row_lds[q];
       const int g = src_lds[q];
       if (g < 0 || g >= T) continue;  // only a layout that does not belong to x gets here
-      dispatch_bf16_unit<BUF_X>(x, [&] { return row; }, recv, g, u - q * chunks, 1, nv, cap, lane);
+      if constexpr (FP8)
+        dispatch_fp8_unit(x, [&] { return row; }, recv, recv_scale, g, u - q * chunks, 1, H, cap, lane);
+      else
+        dispatch_bf16_unit<BUF_X>(x, [&] { return row; }, recv, g, u - q * chunks, 1, H / 8, cap, lane);
     }
     __syncthreads();  // the batch's rows are consumed before the next batch overwrites them
   }
@@ -204,20 +209,23 @@ hipError_t launch_hop_schedule(const int32_t* send_cnt, const int32_t* order, co
 }
 
 hipError_t launch_dispatch_scheduled(const void* x, const int32_t* send_cnt, const int32_t* seg_off,
-                                     const int32_t* recv_src, void* recv, int R, int E, int rows, int n, int64_t T,
-                                     int k, int H, int64_t cap, hipStream_t stream) {
+                                     const int32_t* recv_src, void* recv, float* recv_scale, int R, int E, int rows,
+                                     int n, int64_t T, int k, int H, int64_t cap, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  const int nv = H / 8;
-  const int chunks = (nv + kBf16Cols - 1) / kBf16Cols;
+  const bool fp8 = recv_scale != nullptr;
+  const int chunks = fp8 ? (H + 1023) / 1024 : (H / 8 + kBf16Cols - 1) / kBf16Cols;
   const dim3 grid((unsigned)((int64_t)R * n));
-  if (T * (int64_t)H * 2 >= kBufferLoadXBytes)
-    hipLaunchKernelGGL(dispatch_scheduled_kernel<true>, grid, dim3(kScheduleThreads), 0, stream,
-                       static_cast<const u32x4*>(x), send_cnt, seg_off, recv_src, static_cast<u32x4*>(recv), R, E,
-                       rows, n, T, k, nv, chunks, cap);
+  const u32x4* xv = static_cast<const u32x4*>(x);
+  u32x4* rv = static_cast<u32x4*>(recv);
+  if (fp8)
+    hipLaunchKernelGGL((dispatch_scheduled_kernel<false, true>), grid, dim3(kScheduleThreads), 0, stream, xv, send_cnt,
+                       seg_off, recv_src, rv, recv_scale, R, E, rows, n, T, k, H, chunks, cap);
+  else if (T * (int64_t)H * 2 >= kBufferLoadXBytes)
+    hipLaunchKernelGGL((dispatch_scheduled_kernel<true, false>), grid, dim3(kScheduleThreads), 0, stream, xv, send_cnt,
+                       seg_off, recv_src, rv, nullptr, R, E, rows, n, T, k, H, chunks, cap);
   else
-    hipLaunchKernelGGL(dispatch_scheduled_kernel<false>, grid, dim3(kScheduleThreads), 0, stream,
-                       static_cast<const u32x4*>(x), send_cnt, seg_off, recv_src, static_cast<u32x4*>(recv), R, E,
-                       rows, n, T, k, nv, chunks, cap);
+    hipLaunchKernelGGL((dispatch_scheduled_kernel<false, false>), grid, dim3(kScheduleThreads), 0, stream, xv,
+                       send_cnt, seg_off, recv_src, rv, nullptr, R, E, rows, n, T, k, H, chunks, cap);
   return hipGetLastError();
 }
 

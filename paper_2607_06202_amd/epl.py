@@ -129,7 +129,7 @@ def lib() -> ctypes.CDLL:
         L.epl_hop_schedule.restype = ctypes.c_int
         L.epl_hop_schedule.argtypes = [CP, P, P, I32, P, I32, I32, P, P, P, P]
         L.epl_dispatch_scheduled.restype = ctypes.c_int
-        L.epl_dispatch_scheduled.argtypes = [CP, P, LP, P, I64, I32, I32, P]
+        L.epl_dispatch_scheduled.argtypes = [CP, P, LP, P, P, I64, I32, I32, P]
         _lib = L
     return _lib
 
@@ -600,19 +600,18 @@ def hop_schedule(cfg: Config, send_cnt: torch.Tensor, hop_class: torch.Tensor, w
 
 
 def dispatch_scheduled(cfg: Config, x: torch.Tensor, L: Layout, workers: int, remap_rows: int = 0,
-                       recv: torch.Tensor | None = None) -> torch.Tensor:
+                       recv: torch.Tensor | None = None, recv_scale: torch.Tensor | None = None):
     """epl_dispatch_scheduled: the rows of epl_dispatch, written by one workgroup per (source rank,
-    worker) in the order of the hierarchical token-level schedule -> recv [cap, H] bf16."""
+    worker) in the order of the hierarchical token-level schedule -> (recv [cap, H] bf16 | uint8,
+    recv_scale [cap, H/128] fp32 | None)."""
     dev = x.device
-    if cfg.payload != PAYLOAD_BF16:
-        raise EplError(5, "epl_dispatch_scheduled (bf16 only)")
     _check_layout(cfg, L, dev)
-    recv, _, _, rows = _recv_args(cfg, x, recv, None, dev)
+    recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
     bufs = L.buffers()
     with _on(dev):
-        _check(lib().epl_dispatch_scheduled(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(),
+        _check(lib().epl_dispatch_scheduled(ctypes.byref(cfg), x.data_ptr(), ctypes.byref(bufs), recv.data_ptr(), sp,
                                             rows, remap_rows, workers, _stream(dev)), "epl_dispatch_scheduled")
-    return recv
+    return recv, recv_scale
 
 
 def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):

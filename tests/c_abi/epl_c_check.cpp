@@ -198,7 +198,7 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
     void* d_recv2 = nullptr;
     HIP_OK(hipMalloc(&d_recv2, std::max<size_t>(1, (size_t)Tk * c.H * 2)));
     ok = epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, n, NH, d_se, d_so, d_cnt, stream) == EPL_OK &&
-         epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, Tk, 0, n, stream) == EPL_OK;
+         epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, nullptr, Tk, 0, n, stream) == EPL_OK;
     HIP_OK(hipStreamSynchronize(stream));
     std::vector<uint16_t> rr((size_t)Tk * c.H);
     eplref_dispatch_bf16(T, c.k, c.H, x.data(), r_row.data(), rr.data());
@@ -210,8 +210,8 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
                    EPL_ERR_INVALID_ARG &&
          epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, n, EPL_MAX_HOP_CLASSES + 1, d_se, d_so, d_cnt, stream) ==
              EPL_ERR_INVALID_ARG &&
-         epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, Tk - 1, 0, n, stream) == EPL_ERR_CAPACITY &&
-         epl_dispatch_scheduled(&cfg, (char*)d_x + 2, &L, d_recv2, Tk, 0, n, stream) == EPL_ERR_ALIGN;
+         epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, nullptr, Tk - 1, 0, n, stream) == EPL_ERR_CAPACITY &&
+         epl_dispatch_scheduled(&cfg, (char*)d_x + 2, &L, d_recv2, nullptr, Tk, 0, n, stream) == EPL_ERR_ALIGN;
     HIP_OK(hipFree(d_hop));
     HIP_OK(hipFree(d_se));
     HIP_OK(hipFree(d_so));

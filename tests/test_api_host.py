@@ -349,10 +349,12 @@ def test_schedule_errors_before_any_hip_call(lib):
     L = fake_layout()
     x, recv = Fake.ptr(70), Fake.ptr(71)
 
-    def ds(c=c, x=x, recv=recv, cap=64 * 128 * 8, rows=0, n=32, L=L):
-        return lib.epl_dispatch_scheduled(ctypes.byref(c), x, ctypes.byref(L) if L is not None else None, recv, cap,
-                                          rows, n, None)
-    assert ds(c=epl.config(64, 256, 8, 7168, 128, "fp8")) == UNSUPPORTED
+    def ds(c=c, x=x, recv=recv, sc=None, cap=64 * 128 * 8, rows=0, n=32, L=L):
+        return lib.epl_dispatch_scheduled(ctypes.byref(c), x, ctypes.byref(L) if L is not None else None, recv, sc,
+                                          cap, rows, n, None)
+    assert ds(c=epl.config(64, 256, 8, 7168 + 64, 128, "fp8"), sc=Fake.ptr(72)) == UNSUPPORTED  # H % 128 != 0
+    assert ds(c=epl.config(64, 256, 8, 7168, 128, "fp8")) == INVALID  # no scale buffer
+    assert ds(c=epl.config(64, 256, 8, 7168, 128, "fp8"), sc=Fake.ptr(72, 2)) == ALIGN
     assert ds(n=0) == INVALID
     assert ds(rows=-2) == INVALID
     assert ds(L=None) == INVALID

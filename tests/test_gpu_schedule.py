@@ -155,7 +155,7 @@ def test_dispatch_scheduled_full_size(name):
     idx = W.routing(w)
     cfg, L = run_layout(w, idx, dev)
     x = W.device_normal_bf16((w.T, w.H), 3, dev)
-    a = epl.dispatch_scheduled(cfg, x, L, 32)
+    a, _ = epl.dispatch_scheduled(cfg, x, L, 32)
     b, _ = epl.dispatch(cfg, x, L)
     torch.cuda.synchronize()
     P = int(L.expert_off[-1].item())
@@ -164,3 +164,35 @@ def test_dispatch_scheduled_full_size(name):
         hi = min(P, lo + (1 << 14))
         assert torch.equal(a[lo:hi].view(torch.int16), x[src[lo:hi]].view(torch.int16)), (name, lo)
         assert torch.equal(a[lo:hi].view(torch.int16), b[lo:hi].view(torch.int16)), (name, lo)
+
+
+@pytest.mark.parametrize("R,E,k,Tr,H,seed,workers,rows", [
+    (4, 16, 3, 24, 256, 0, 4, 0), (64, 256, 8, 4, 7168, 1, 16, 8), (2, 4, 5, 30, 1152, 2, 7, 1),
+])
+def test_dispatch_scheduled_fp8_parity(R, E, k, Tr, H, seed, workers, rows):
+    """fp8 payloads: every packed row's codes and scales, bit for bit against the oracle's quantiser."""
+    dev = device()
+    T = R * Tr
+    idx = W.with_replacement(seed, T, k, -1, E + 1).astype(np.int32)
+    x = W.normal_bf16(seed, W.STREAM_X, T * H).reshape(T, H)
+    w = W.Workload("d", R, E, k, Tr, H, "fp8", "-")
+    cfg, L = run_layout(w, idx, dev)
+    recv, scale = epl.dispatch_scheduled(cfg, to_dev_bf16(x, dev), L, workers, remap_rows=rows)
+    torch.cuda.synchronize()
+    ref = oracle.layout(R, E, k, Tr, idx)
+    q, s = oracle.dispatch_fp8(x, ref.pair_row, ref.P)
+    np.testing.assert_array_equal(recv[:ref.P].cpu().numpy(), q)
+    np.testing.assert_array_equal(scale[:ref.P].cpu().numpy().view(np.uint32), s.view(np.uint32))
+
+
+def test_dispatch_scheduled_fp8_full_size_skewed():
+    """The skewed fp8 workload: every packed row and scale equal to epl_dispatch's."""
+    dev = device()
+    w = W.WORKLOADS["skewed_fp8_ep64"]
+    cfg, L = run_layout(w, W.routing(w), dev)
+    x = W.device_normal_bf16((w.T, w.H), 4, dev)
+    a, sa = epl.dispatch_scheduled(cfg, x, L, 64, remap_rows=8)
+    b, sb = epl.dispatch(cfg, x, L)
+    torch.cuda.synchronize()
+    P = int(L.expert_off[-1].item())
+    assert torch.equal(a[:P], b[:P]) and torch.equal(sa[:P].view(torch.int32), sb[:P].view(torch.int32))
