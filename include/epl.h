@@ -313,7 +313,8 @@ epl_status epl_locate_rows(const epl_config *cfg, const int32_t *expert_off, con
  *              column by column, skipping empty cells. remap_rows 0 means one row per worker
  *              (remap_rows = workers); remap_rows 1 gives the natural order 0..E-1. An order entry
  *              outside [0, E) counts as an expert with no pairs.
- *   send_cnt   [R*E] int32 device, a layout's send_cnt (or any non-negative counts).
+ *   send_cnt   [R*E] int32 device, a layout's send_cnt, or any non-negative counts whose sum per rank
+ *              stays below 2^31 (other values give unspecified but in-bounds results).
  *   hop_class  [R*R] int32 device, hop class of each (source, destination rank).
  * workers >= 1 and R*workers < 2^31; 1 <= num_classes <= EPL_MAX_HOP_CLASSES; remap_rows >= 0
  * (INVALID_ARG otherwise); pointers 4-byte aligned (ALIGN). One launch of R workgroups.        */
