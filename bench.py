@@ -408,6 +408,9 @@ def main():
                          "sending one equal slice of the rank's pairs in the transposed expert order) + epl_combine")
     ap.add_argument("--remap-rows", type=int, default=0,
                     help="rows of the expert transposition of --scheduled (0: one per worker; 1: natural order)")
+    ap.add_argument("--shape", type=int, nargs=5, metavar=("R", "E", "K", "TR", "H"),
+                    help="a custom bf16 workload with uniform routing instead of --workload: R ranks, E experts, "
+                         "top-K, TR tokens per rank, hidden size H")
     ap.add_argument("--count-groups", type=int, default=0,
                     help="count workgroups of the decomposed launch (0: the library's default split)")
     ap.add_argument("--graph", action="store_true",
@@ -465,7 +468,11 @@ def main():
                           "GBps": 2 * n / ms / 1e6}))
         return
 
-    w = W.WORKLOADS[args.workload]
+    if args.shape:
+        R, E, K, TR, H = args.shape
+        w = W.Workload("custom_r%d_e%d_k%d_t%d_h%d" % (R, E, K, TR, H), R, E, K, TR, H, "bf16", "uniform")
+    else:
+        w = W.WORKLOADS[args.workload]
     dinfo = device_info(torch)  # read before the run: the temperatures are those at the start
     if args.calibrate_replicate:
         calibrate_replicate(torch, epl, w, dev, stream, args.steps)
