@@ -417,6 +417,9 @@ def main():
                     help="time HIP graph replays of the layer (one graph per x copy) instead of eager launches")
     ap.add_argument("--recv-alloc", choices=["contiguous", "torch"], default="contiguous",
                     help="receive buffer: one physically contiguous HIP block (default) or torch's allocator")
+    ap.add_argument("--row-pitch", default="auto",
+                    help="elements from one receive row to the next: 'auto' (the library's padded pitch: H + 768 "
+                         "for bf16 rows of 7168, packed rows for fp8), 0 (packed, H) or a multiple of 64 >= H")
     ap.add_argument("--warm", action="store_true",
                     help="read the same x every step (it may stay in the memory-side cache) instead of rotating copies")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
@@ -480,7 +483,8 @@ def main():
     idx = W.routing(w, args.seed)
     x = W.tokens_bf16(w, args.seed)
     gw = W.gate_weights(w, args.seed)
-    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)
+    pitch = epl.padded_pitch(w.H, w.payload) if args.row_pitch == "auto" else int(args.row_pitch)
+    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload, row_pitch=pitch)
 
     idx_d = torch.from_numpy(idx).to(dev)
     x_d = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
@@ -506,7 +510,7 @@ def main():
     if w.payload == "fp8":
         # combine reads bf16 expert outputs; identity experts would dequantise -- here a bf16
         # buffer of the same shape stands in for them (not timed)
-        y = torch.zeros(epl.recv_rows_cap(cfg), w.H, dtype=torch.bfloat16, device=dev)
+        y = torch.zeros(epl.recv_rows_cap(cfg), cfg.pitch, dtype=torch.bfloat16, device=dev)[:, :w.H]
     else:
         y = recv
 
@@ -755,7 +759,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": w.payload, "data": "synthetic",
         "config": {"workload": w.name, "ranks": w.R, "experts": w.E, "topk": w.k, "tokens_per_rank": w.T // w.R,
-                   "hidden": w.H, "payload": w.payload, "routing": w.routing, "pairs": P, "seed": args.seed},
+                   "hidden": w.H, "payload": w.payload, "routing": w.routing, "pairs": P, "seed": args.seed,
+                   "row_pitch": cfg.pitch},
         "us_per_layer": round(ms_per_step * 1e3, 2), "us_per_layer_instrumented": round(us_layer_events, 2),
         "us_layout": round(us_layout, 2), "us_dispatch": round(us_dispatch, 2),
         "us_layout_dispatch": round(us_dispatch + us_layout, 2),

@@ -23,6 +23,12 @@
  * Receive layout:
  *   - The valid pairs, stably sorted by expert id, take packed rows 0..P-1.
  *   - So rows run in (destination rank, expert, source rank, token, j) order, with no gaps.
+ *   - Row r of recv, and of the expert outputs y that combine reads, starts at element r*pitch,
+ *     where pitch = row_pitch, or H when row_pitch is 0. Elements [H, pitch) of a row are never
+ *     read or written. A pitch a little above H can be faster than H itself: on MI355X, with
+ *     H = 7168 bf16 (14 KiB rows), a pitch of H + 768 (15.5 KiB) took 1-4% off the layer at 64
+ *     ranks and 8192 tokens and changed nothing measurable at larger sizes, while H + 1024
+ *     (16 KiB, a power of two) made it 2% slower.
  *
  * Conventions:
  *   - Every pointer argument is a DEVICE pointer unless stated. The caller allocates and owns
@@ -72,6 +78,8 @@ typedef struct {
   int32_t hidden;          /* 8 <= H <= EPL_MAX_HIDDEN, H % 8 == 0; H % 128 == 0 for fp8 */
   int32_t tokens_per_rank; /* Tr >= 0; T*k < 2^31                                        */
   int32_t payload;         /* epl_payload: dispatch output format                        */
+  int32_t row_pitch;       /* elements from one recv (and y) row to the next; 0 means H;
+                              otherwise H <= row_pitch <= EPL_MAX_HIDDEN, row_pitch % 64 == 0 */
 } epl_config;
 
 /* Layout outputs: int32 device arrays, caller-allocated, all required (non-NULL).
@@ -126,8 +134,9 @@ epl_status epl_layout(const epl_config *cfg, const int32_t *topk_idx, const epl_
  * offsets are known before any row is written).
  *   x          [T*H] bf16 bit patterns, row-major, read-only; must not alias recv.
  *   L          a layout produced by epl_layout for the same cfg (pair_row is read).
- *   recv       [recv_rows_cap * H] elements: bf16 (2 bytes) for EPL_PAYLOAD_BF16, or E4M3
- *              bytes for EPL_PAYLOAD_FP8_E4M3. Rows 0..P-1 are written, rows >= P untouched.
+ *   recv       recv_rows_cap rows of pitch elements (the last row may end after its H-th):
+ *              bf16 (2 bytes) for EPL_PAYLOAD_BF16, or E4M3 bytes for EPL_PAYLOAD_FP8_E4M3.
+ *              Elements 0..H-1 of rows 0..P-1 are written; nothing else is touched.
  *   recv_scale fp8 only: [recv_rows_cap * H/128] fp32. Scale b of a row covers columns
  *              [128b, 128b+128): s = max|x| / 448 over the block (IEEE fp32 division),
  *              q = E4M3(x / s) rounded to nearest-even with saturation to +-448, sign kept on
@@ -223,9 +232,9 @@ int epl_decomposed_plan(const epl_config *cfg, int32_t count_groups, int32_t *gr
  * the offsets, work out each token's rows, and load each 16-byte piece of a row with device-scope
  * loads until none of its elements is EPL_SENTINEL_BF16, fold it (the arithmetic of epl_combine,
  * bit for bit), and write the sentinel back over it (the reset after consumption).
- *   recv       [recv_rows_cap * H] bf16: every element must hold EPL_SENTINEL_BF16 before the
- *              first call (epl_sentinel_fill); each call leaves it so. No other call may write it
- *              in between.
+ *   recv       recv_rows_cap rows of pitch bf16 elements: elements 0..H-1 of every row must hold
+ *              EPL_SENTINEL_BF16 before the first call (epl_sentinel_fill over the whole buffer);
+ *              each call leaves them so. No other call may write them in between.
  *   x          must not hold EPL_SENTINEL_BF16 (check with epl_sentinel_find at initialisation); a
  *              row that does is reported (EPL_WAIT_SENTINEL_IN_X) and its combine gives up.
  *   topk_w, out  as epl_combine (out [T*H] bf16 = the combine of x's rows).
@@ -266,7 +275,8 @@ epl_status epl_layout_dispatch_noalloc(const epl_config *cfg, const int32_t *top
 
 /* Combine: gate-weighted gather-reduce of expert output rows back into token order (the
  * paper's combine: gather expert outputs, restore token order).
- *   y       [>= P rows][H] bf16 expert outputs, row r holds the expert result for packed row r.
+ *   y       >= P rows of pitch bf16 elements (the receive layout's pitch): elements 0..H-1 of
+ *           row r hold the expert result for packed row r.
  *   topk_w  [T*k] fp32 gate weights, applied as given (no renormalisation).
  *   out     [T*H] bf16. For every token g and column c:
  *             acc = +0.0f; for j = 0..k-1 with pair_row[g*k+j] >= 0:

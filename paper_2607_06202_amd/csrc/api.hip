@@ -25,9 +25,14 @@ epl_status check_config(const epl_config* cfg) {
   if (R < 1 || E < R || E > EPL_MAX_EXPERTS || E % R != 0) return EPL_ERR_INVALID_ARG;
   if (k < 1 || k > EPL_MAX_TOPK || Tr < 0 || H < 8 || H > EPL_MAX_HIDDEN || H % 8 != 0) return EPL_ERR_INVALID_ARG;
   if ((int64_t)R * Tr * k >= (int64_t)INT_MAX) return EPL_ERR_INVALID_ARG;
+  const int P = cfg->row_pitch;
+  if (P != 0 && (P < H || P > EPL_MAX_HIDDEN || P % 64 != 0)) return EPL_ERR_INVALID_ARG;
   if (cfg->payload != EPL_PAYLOAD_BF16 && cfg->payload != EPL_PAYLOAD_FP8_E4M3) return EPL_ERR_UNSUPPORTED;
   return EPL_OK;
 }
+
+// Elements from one receive (and expert-output) row to the next.
+int pitch_of(const epl_config* cfg) { return cfg->row_pitch ? cfg->row_pitch : cfg->hidden; }
 
 // Chunking of each source rank's tokens for the layout kernels: whole tokens, at most
 // kMaxChunkPairs pairs per workgroup.
@@ -129,10 +134,12 @@ hipError_t run_rows(const epl::Geom& g, const epl_config* cfg, const int32_t* to
                     int32_t* ws, const void* x, void* recv, float* recv_scale, int64_t cap, hipStream_t s) {
   if (rows_fused(g, cfg))
     return epl::launch_fused_dispatch(g, topk_idx, ws, L->expert_off, L->rank_off, L->seg_off, L->pair_row,
-                                      L->pair_rslot, L->recv_src, L->recv_j, x, recv, cfg->hidden, cap, s);
+                                      L->pair_rslot, L->recv_src, L->recv_j, x, recv, cfg->hidden, pitch_of(cfg),
+                                      cap, s);
   if (cfg->payload == EPL_PAYLOAD_FP8_E4M3)
-    return epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden, cap, s);
-  return epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, cap, s);
+    return epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, g.T, cfg->topk, cfg->hidden, pitch_of(cfg),
+                                    cap, s);
+  return epl::launch_dispatch_bf16(x, L->pair_row, recv, g.T, cfg->topk, cfg->hidden, pitch_of(cfg), cap, s);
 }
 
 }  // namespace
@@ -161,8 +168,9 @@ EPL_EXPORT epl_status epl_dispatch(const epl_config* cfg, const void* x, const e
   if (recv_rows_cap < T * cfg->topk) return EPL_ERR_CAPACITY;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (fp8) return from_hip(epl::launch_dispatch_fp8(x, L->pair_row, recv, recv_scale, T, cfg->topk, cfg->hidden,
-                                                   recv_rows_cap, s));
-  return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, T, cfg->topk, cfg->hidden, recv_rows_cap, s));
+                                                   pitch_of(cfg), recv_rows_cap, s));
+  return from_hip(epl::launch_dispatch_bf16(x, L->pair_row, recv, T, cfg->topk, cfg->hidden, pitch_of(cfg),
+                                            recv_rows_cap, s));
 }
 
 
@@ -234,7 +242,8 @@ EPL_EXPORT epl_status epl_layout_dispatch_decomposed(const epl_config* cfg, cons
   if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, false, &plan) != hipSuccess) return EPL_ERR_DEVICE;
   if (plan.grid > plan.capacity) return EPL_ERR_UNSUPPORTED;
   return from_hip(epl::launch_decomposed(g, topk_idx, static_cast<int32_t*>(workspace), *L, x, recv, cfg->hidden,
-                                         recv_rows_cap, o, wait_status, static_cast<hipStream_t>(stream)));
+                                         pitch_of(cfg), recv_rows_cap, o, wait_status,
+                                         static_cast<hipStream_t>(stream)));
 }
 
 EPL_EXPORT int epl_decomposed_plan(const epl_config* cfg, int32_t count_groups, int32_t* grid, int32_t* capacity) {
@@ -263,8 +272,8 @@ EPL_EXPORT epl_status epl_layer_sentinel(const epl_config* cfg, const int32_t* t
   if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, true, &plan) != hipSuccess) return EPL_ERR_DEVICE;
   if (plan.grid > plan.capacity) return EPL_ERR_UNSUPPORTED;
   return from_hip(epl::launch_decomposed(g, topk_idx, static_cast<int32_t*>(workspace), *L, x, recv, cfg->hidden,
-                                         recv_rows_cap, o, wait_status, static_cast<hipStream_t>(stream), topk_w,
-                                         out));
+                                         pitch_of(cfg), recv_rows_cap, o, wait_status,
+                                         static_cast<hipStream_t>(stream), topk_w, out));
 }
 
 EPL_EXPORT epl_status epl_sentinel_fill(void* buf, int64_t n, void* stream) {
@@ -395,7 +404,8 @@ EPL_EXPORT epl_status epl_dispatch_scheduled(const epl_config* cfg, const void* 
   return from_hip(epl::launch_dispatch_scheduled(x, L->send_cnt, L->seg_off, L->recv_src, recv,
                                                  fp8 ? recv_scale : nullptr, cfg->num_ranks, cfg->num_experts,
                                                  remap_rows ? remap_rows : workers, workers, T, cfg->topk,
-                                                 cfg->hidden, recv_rows_cap, static_cast<hipStream_t>(stream)));
+                                                 cfg->hidden, pitch_of(cfg), recv_rows_cap,
+                                                 static_cast<hipStream_t>(stream)));
 }
 
 EPL_EXPORT epl_status epl_combine(const epl_config* cfg, const void* y, const float* topk_w,
@@ -407,7 +417,7 @@ EPL_EXPORT epl_status epl_combine(const epl_config* cfg, const void* y, const fl
   const int64_t T = (int64_t)cfg->num_ranks * cfg->tokens_per_rank;
   if (T > 0 && (!y || !topk_w || !out)) return EPL_ERR_INVALID_ARG;
   if (!aligned(y, 16) || !aligned(out, 16) || !aligned(topk_w, 4)) return EPL_ERR_ALIGN;
-  return from_hip(epl::launch_combine(y, topk_w, L->pair_row, out, T, cfg->topk, cfg->hidden,
+  return from_hip(epl::launch_combine(y, topk_w, L->pair_row, out, T, cfg->topk, cfg->hidden, pitch_of(cfg),
                                       static_cast<hipStream_t>(stream)));
 }
 

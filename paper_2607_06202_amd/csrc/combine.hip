@@ -29,7 +29,8 @@ constexpr int combine_cols() { return kWave * VPL; }
 // fmaf. Larger k walks the choices in groups of kGather, still in j order.
 template <bool SMALL_K, int VPL>
 __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const int32_t* rows, const float* ws,
-                                             u32x4* __restrict__ out, int64_t g, int c, int k, int nv, int lane) {
+                                             u32x4* __restrict__ out, int64_t g, int c, int k, int nv, int pv,
+                                             int lane) {
   int v[VPL], vl[VPL];
 #pragma unroll
   for (int q = 0; q < VPL; ++q) {
@@ -50,7 +51,7 @@ __device__ __forceinline__ void combine_unit(const u32x4* __restrict__ y, const 
       const int row = j < k ? __builtin_amdgcn_readfirstlane(rows[j]) : -1;
       if (row >= 0) {
 #pragma unroll
-        for (int q = 0; q < VPL; ++q) buf[jj][q] = __builtin_nontemporal_load(y + (int64_t)row * nv + vl[q]);
+        for (int q = 0; q < VPL; ++q) buf[jj][q] = __builtin_nontemporal_load(y + (int64_t)row * pv + vl[q]);
       }
     }
 #pragma unroll
@@ -109,7 +110,7 @@ template <bool SMALL_K, int VPL>
 __global__ void __launch_bounds__(kCombineThreads)
     __attribute__((amdgpu_waves_per_eu(combine_waves_per_simd(VPL), combine_waves_per_simd(VPL))))
     combine_kernel(const u32x4* __restrict__ y, const float* __restrict__ w, const int32_t* __restrict__ pair_row,
-                   u32x4* __restrict__ out, int64_t T, int k, int nv, int chunks) {
+                   u32x4* __restrict__ out, int64_t T, int k, int nv, int pv, int chunks) {
   __shared__ int32_t rows_lds[kCombineWaves * EPL_MAX_TOPK];
   __shared__ float w_lds[kCombineWaves * EPL_MAX_TOPK];
   const int64_t units = T * chunks;
@@ -128,34 +129,34 @@ __global__ void __launch_bounds__(kCombineThreads)
     if (unit >= units) continue;
     const int64_t g = unit / chunks;
     combine_unit<SMALL_K, VPL>(y, rows_lds + (g - g_first) * k, w_lds + (g - g_first) * k, out, g,
-                          (int)(unit - g * chunks), k, nv, lane);
+                          (int)(unit - g * chunks), k, nv, pv, lane);
   }
 }
 
 template <int VPL>
 void launch_combine_vpl(const u32x4* y, const float* w, const int32_t* pair_row, u32x4* out, int64_t T, int k, int nv,
-                        hipStream_t stream) {
+                        int pv, hipStream_t stream) {
   const int chunks = (nv + combine_cols<VPL>() - 1) / combine_cols<VPL>();
   const int64_t blocks = (T * chunks + kCombineWaves - 1) / kCombineWaves;
   const dim3 grid((unsigned)std::min<int64_t>(blocks, 1 << 30));
   if (k <= kGather)
     hipLaunchKernelGGL((combine_kernel<true, VPL>), grid, dim3(kCombineThreads), 0, stream, y, w, pair_row, out, T, k,
-                       nv, chunks);
+                       nv, pv, chunks);
   else
     hipLaunchKernelGGL((combine_kernel<false, VPL>), grid, dim3(kCombineThreads), 0, stream, y, w, pair_row, out, T, k,
-                       nv, chunks);
+                       nv, pv, chunks);
 }
 
 hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
-                          int H, hipStream_t stream) {
+                          int H, int pitch, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const int nv = H / 8;
   const u32x4* yv = static_cast<const u32x4*>(y);
   u32x4* ov = static_cast<u32x4*>(out);
   if (T * k * (int64_t)H * 2 >= kWideCombineBytes)
-    launch_combine_vpl<2>(yv, w, pair_row, ov, T, k, nv, stream);
+    launch_combine_vpl<2>(yv, w, pair_row, ov, T, k, nv, pitch / 8, stream);
   else
-    launch_combine_vpl<1>(yv, w, pair_row, ov, T, k, nv, stream);
+    launch_combine_vpl<1>(yv, w, pair_row, ov, T, k, nv, pitch / 8, stream);
   return hipGetLastError();
 }
 

@@ -64,7 +64,7 @@ struct DecomposedArgs {
   int cchunks, nco;            // 1 KiB column chunks per row; combine workgroups
   const u32x4* x;
   u32x4* recv;
-  int nv, chunks;
+  int nv, pv, chunks;          // x row and recv pitch in 16-byte vectors; 4 KiB chunks per row
   int64_t cap;
   int nc, ns;                  // count and send workgroups
   int32_t* sync;               // [kSyncWords]
@@ -182,7 +182,7 @@ __device__ __forceinline__ void send_role(const DecomposedArgs& A, int j, int32_
           __syncthreads();  // every wave has its rows before the next iteration rewrites them
           return r;
         },
-        A.recv, g, c, k, A.nv, A.cap, lane, active, [&](const u32x4* buf, const bool* on) {
+        A.recv, g, c, k, A.nv, A.pv, A.cap, lane, active, [&](const u32x4* buf, const bool* on) {
           if constexpr (LAYER) {
             bool seen = false;
 #pragma unroll
@@ -269,7 +269,7 @@ __device__ __forceinline__ void combine_role(const DecomposedArgs& A, int ci, in
       if (row < 0) continue;
       const float wj = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
                                                       __builtin_bit_cast(int, A.topk_w[g * k + j])));
-      const u32x4* yr = y + (int64_t)row * nv;
+      const u32x4* yr = y + (int64_t)row * A.pv;
       u32x4 val;
       if (!poll_vec(yr, nv, vl, val, A.spin_ticks)) {
         arrived = false;
@@ -379,7 +379,7 @@ hipError_t plan_decomposed(const Geom& g, int H, int count_groups, bool layer, D
 }
 
 hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, const epl_layout_buffers& L,
-                             const void* x, void* recv, int H, int64_t cap, const DecomposedOpts& opts,
+                             const void* x, void* recv, int H, int pitch, int64_t cap, const DecomposedOpts& opts,
                              int32_t* wait_status, hipStream_t stream, const float* topk_w, void* out) {
   const bool layer = out != nullptr;
   DecomposedPlan plan;
@@ -408,6 +408,7 @@ hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, con
   A.x = static_cast<const u32x4*>(x);
   A.recv = static_cast<u32x4*>(recv);
   A.nv = H / 8;
+  A.pv = pitch / 8;
   A.chunks = (A.nv + kBf16Cols - 1) / kBf16Cols;
   A.cchunks = (A.nv + kWave - 1) / kWave;
   A.cap = cap;

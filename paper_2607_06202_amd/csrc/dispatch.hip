@@ -31,14 +31,15 @@ template <bool BUF_X>
 __global__ void __launch_bounds__(kPlainThreads)
     __attribute__((amdgpu_waves_per_eu(bf16_min_waves(BUF_X), bf16_max_waves(BUF_X))))
     dispatch_bf16_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
-                         int64_t T, int k, int nv, int chunks, int64_t cap) {
+                         int64_t T, int k, int nv, int pv, int chunks, int64_t cap) {
   const int lane = threadIdx.x % kWave;
   const int64_t units = T * chunks;
   const int64_t stride = (int64_t)gridDim.x * kPlainWaves;
   for (int64_t u = (int64_t)blockIdx.x * kPlainWaves + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / chunks;
     dispatch_bf16_unit<BUF_X>(
-        x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, g, (int)(u - g * chunks), k, nv, cap, lane);
+        x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, g, (int)(u - g * chunks), k, nv, pv, cap,
+        lane);
   }
 }
 
@@ -57,19 +58,19 @@ __global__ void __launch_bounds__(kPlainThreads)
 constexpr int kFp8WavesPerSimd = 3;
 __global__ void __launch_bounds__(kFp8Threads) __attribute__((amdgpu_waves_per_eu(kFp8WavesPerSimd, kFp8WavesPerSimd)))
     dispatch_fp8_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ pair_row, u32x4* __restrict__ recv,
-                        float* __restrict__ recv_scale, int64_t T, int k, int H, int npass, int64_t cap) {
+                        float* __restrict__ recv_scale, int64_t T, int k, int H, int pq, int npass, int64_t cap) {
   const int lane = threadIdx.x % kWave;
   const int64_t units = T * npass;
   const int64_t stride = (int64_t)gridDim.x * kFp8Waves;
   for (int64_t u = (int64_t)blockIdx.x * kFp8Waves + threadIdx.x / kWave; u < units; u += stride) {
     const int64_t g = u / npass;
     dispatch_fp8_unit(x, [&] { return lane < k ? pair_row[g * k + lane] : -1; }, recv, recv_scale, g,
-                      (int)(u - g * npass), k, H, cap, lane);
+                      (int)(u - g * npass), k, H, pq, cap, lane);
   }
 }
 
 hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* recv, int64_t T, int k, int H,
-                                int64_t cap, hipStream_t stream) {
+                                int pitch, int64_t cap, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const int nv = H / 8;
   const int chunks = (nv + kBf16Cols - 1) / kBf16Cols;
@@ -77,21 +78,23 @@ hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* re
   const dim3 grid((unsigned)std::min<int64_t>((units + kPlainWaves - 1) / kPlainWaves, 1 << 30));
   if (T * (int64_t)H * 2 >= kBufferLoadXBytes)
     hipLaunchKernelGGL(dispatch_bf16_kernel<true>, grid, dim3(kPlainThreads), 0, stream,
-                       static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
+                       static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, pitch / 8, chunks,
+                       cap);
   else
     hipLaunchKernelGGL(dispatch_bf16_kernel<false>, grid, dim3(kPlainThreads), 0, stream,
-                       static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, chunks, cap);
+                       static_cast<const u32x4*>(x), pair_row, static_cast<u32x4*>(recv), T, k, nv, pitch / 8, chunks,
+                       cap);
   return hipGetLastError();
 }
 
 hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* recv, float* recv_scale, int64_t T,
-                               int k, int H, int64_t cap, hipStream_t stream) {
+                               int k, int H, int pitch, int64_t cap, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const int npass = (H + 1023) / 1024;
   const int64_t units = T * npass;
   const dim3 grid((unsigned)std::min<int64_t>((units + kFp8Waves - 1) / kFp8Waves, 1 << 30));
   hipLaunchKernelGGL(dispatch_fp8_kernel, grid, dim3(kFp8Threads), 0, stream, static_cast<const u32x4*>(x),
-                     pair_row, static_cast<u32x4*>(recv), recv_scale, T, k, H, npass, cap);
+                     pair_row, static_cast<u32x4*>(recv), recv_scale, T, k, H, pitch / 16, npass, cap);
   return hipGetLastError();
 }
 
@@ -115,8 +118,8 @@ hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* rec
 // flight while it runs.
 template <bool BUF_X>
 __global__ void __launch_bounds__(kDispatchThreads)
-    fused_bf16_kernel(FusedLayout F, const u32x4* __restrict__ x, u32x4* __restrict__ recv, int nv, int chunks,
-                      int64_t cap, int unit_grid, int nmeta) {
+    fused_bf16_kernel(FusedLayout F, const u32x4* __restrict__ x, u32x4* __restrict__ recv, int nv, int pv,
+                      int chunks, int64_t cap, int unit_grid, int nmeta) {
   extern __shared__ int32_t lds[];
   // The metadata workgroups come first in the grid, so that they run alongside the units
   // instead of after them.
@@ -153,7 +156,7 @@ __global__ void __launch_bounds__(kDispatchThreads)
           __syncthreads();  // every wave has its rows before the next iteration rewrites them
           return r;
         },
-        recv, g, c, k, nv, cap, lane, active);
+        recv, g, c, k, nv, pv, cap, lane, active);
   }
 }
 
@@ -163,8 +166,8 @@ bool fused_dispatch_ok(const Geom& g, bool fp8) {
 
 hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* expert_off,
                                  int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
-                                 int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int64_t cap,
-                                 hipStream_t stream) {
+                                 int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int pitch,
+                                 int64_t cap, hipStream_t stream) {
   const WsLayout wl = ws_layout(g);
   const FusedLayout F{g,          idx,          ws + wl.chunk_e, ws + wl.chunk_r,
                       ws + wl.recv_cnt, ws + wl.seg_rel, reinterpret_cast<const uint32_t*>(ws + wl.fmask),
@@ -181,11 +184,11 @@ hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws,
   const u32x4* xv = static_cast<const u32x4*>(x);
   u32x4* rv = static_cast<u32x4*>(recv);
   if (buf_x)
-    hipLaunchKernelGGL(fused_bf16_kernel<true>, grid, dim3(kDispatchThreads), lds, stream, F, xv, rv, H / 8, chunks,
-                       cap, unit_grid, nmeta);
+    hipLaunchKernelGGL(fused_bf16_kernel<true>, grid, dim3(kDispatchThreads), lds, stream, F, xv, rv, H / 8,
+                       pitch / 8, chunks, cap, unit_grid, nmeta);
   else
-    hipLaunchKernelGGL(fused_bf16_kernel<false>, grid, dim3(kDispatchThreads), lds, stream, F, xv, rv, H / 8, chunks,
-                       cap, unit_grid, nmeta);
+    hipLaunchKernelGGL(fused_bf16_kernel<false>, grid, dim3(kDispatchThreads), lds, stream, F, xv, rv, H / 8,
+                       pitch / 8, chunks, cap, unit_grid, nmeta);
   return hipGetLastError();
 }
 

@@ -265,17 +265,18 @@ hipError_t launch_layout(const Geom& g, const int32_t* idx, int32_t* ws, int32_t
                          int32_t* pair_row, int32_t* pair_rslot, int32_t* recv_src, int32_t* recv_j,
                          int32_t* num_invalid, hipStream_t stream);
 
+// pitch: elements from one recv row to the next (>= H, a multiple of 64).
 hipError_t launch_dispatch_bf16(const void* x, const int32_t* pair_row, void* recv, int64_t T, int k, int H,
-                                int64_t cap, hipStream_t stream);
+                                int pitch, int64_t cap, hipStream_t stream);
 hipError_t launch_dispatch_fp8(const void* x, const int32_t* pair_row, void* recv, float* recv_scale, int64_t T,
-                               int k, int H, int64_t cap, hipStream_t stream);
+                               int k, int H, int pitch, int64_t cap, hipStream_t stream);
 // The layout's finalize step fused into the bf16 dispatch (after launch_layout_counts on the same
 // stream), for the geometries fused_dispatch_ok accepts.
 bool fused_dispatch_ok(const Geom& g, bool fp8);
 hipError_t launch_fused_dispatch(const Geom& g, const int32_t* idx, int32_t* ws, int32_t* expert_off,
                                  int32_t* rank_off, int32_t* seg_off, int32_t* pair_row, int32_t* pair_rslot,
-                                 int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int64_t cap,
-                                 hipStream_t stream);
+                                 int32_t* recv_src, int32_t* recv_j, const void* x, void* recv, int H, int pitch,
+                                 int64_t cap, hipStream_t stream);
 // The decomposed single-launch layout and dispatch (bf16, the geometries fused_dispatch_ok
 // accepts). count_groups 0 picks the default split; spin_ticks bounds every wait (100 MHz ticks);
 // ready_target is the published value the send workgroups wait for (1; a test passes 2 to force a
@@ -294,13 +295,14 @@ hipError_t plan_decomposed(const Geom& g, int H, int count_groups, bool layer, D
 // With out != nullptr, the layer variant: combine workgroups gather the rows into out with the
 // weights topk_w as the send workgroups write them.
 hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, const epl_layout_buffers& L,
-                             const void* x, void* recv, int H, int64_t cap, const DecomposedOpts& opts,
+                             const void* x, void* recv, int H, int pitch, int64_t cap, const DecomposedOpts& opts,
                              int32_t* wait_status, hipStream_t stream, const float* topk_w = nullptr,
                              void* out = nullptr);
 // Every 16-byte vector of buf [nvec] set to the bf16 sentinel.
 hipError_t launch_sentinel_fill(void* buf, int64_t nvec, hipStream_t stream);
+// y rows are pitch elements apart.
 hipError_t launch_combine(const void* y, const float* w, const int32_t* pair_row, void* out, int64_t T, int k,
-                          int H, hipStream_t stream);
+                          int H, int pitch, hipStream_t stream);
 
 hipError_t launch_locate_rows(const int32_t* expert_off, const int32_t* rows, int64_t n, int E, int32_t* expert,
                               int32_t* offset, hipStream_t stream);
@@ -310,7 +312,7 @@ hipError_t launch_hop_schedule(const int32_t* send_cnt, const int32_t* order, co
 // recv_scale non-null: fp8 payload (rows quantised as in launch_dispatch_fp8).
 hipError_t launch_dispatch_scheduled(const void* x, const int32_t* send_cnt, const int32_t* seg_off,
                                      const int32_t* recv_src, void* recv, float* recv_scale, int R, int E, int rows,
-                                     int n, int64_t T, int k, int H, int64_t cap, hipStream_t stream);
+                                     int n, int64_t T, int k, int H, int pitch, int64_t cap, hipStream_t stream);
 hipError_t launch_debug_e4m3(const float* in, uint8_t* out, int64_t n, hipStream_t stream);
 hipError_t launch_debug_bf16(const float* in, uint16_t* out, int64_t n, hipStream_t stream);
 

@@ -38,7 +38,8 @@ __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int
 }
 
 // bf16: unit = (token g, column chunk c). The wave loads its chunk of x[g] once and stores it
-// to the k destination rows, interleaving destinations per vector.
+// to the k destination rows, interleaving destinations per vector. x rows are nv vectors apart,
+// recv rows pv (the receive pitch in 16-byte vectors).
 //
 // BUF_X selects how x is read, both with the default cache policy: buffer loads through a
 // resource bounded to the row, or plain global loads. Measured over three repetitions each
@@ -57,7 +58,7 @@ struct NoCheck {
 };
 template <bool BUF_X, class RowFn, class CheckFn = NoCheck>
 __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
-                                                   int64_t g, int c, int k, int nv, int64_t cap, int lane,
+                                                   int64_t g, int c, int k, int nv, int pv, int64_t cap, int lane,
                                                    bool active = true, CheckFn check = CheckFn()) {
   const u32x4* xr = x + g * nv;
   const int v0 = c * kBf16Cols + lane;
@@ -85,7 +86,7 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
     for (int j = 0; j < k; ++j) {
       const int row = __builtin_amdgcn_readlane(my_row, j);
       if (row < 0 || row >= cap) continue;
-      if (v < nv) store_row_policy<kCachePolicySc1>(buf[u], recv + (int64_t)row * nv, nv, v);
+      if (v < nv) store_row_policy<kCachePolicySc1>(buf[u], recv + (int64_t)row * pv, nv, v);
     }
   }
 }
@@ -94,10 +95,11 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
 // elements [16l, 16l+16) of the pass: two 16-byte bf16 loads -> one 16-byte E4M3 store per
 // destination. A 128-element block spans 8 lanes, whose max is combined with three
 // xor-shuffles; the first lane of each block stores that block's scale for every destination.
+// recv rows are pq 16-byte vectors apart (the receive pitch, in bytes / 16).
 template <class RowFn>
 __device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
                                                   float* __restrict__ recv_scale, int64_t g, int p, int k, int H,
-                                                  int64_t cap, int lane) {
+                                                  int pq, int64_t cap, int lane) {
   const int NB = H / 128;
   const int nvq = H / 16;  // 16-byte fp8 vectors per row
   const u32x4* xr = x + g * (H / 8);
@@ -133,7 +135,7 @@ __device__ __forceinline__ void dispatch_fp8_unit(const u32x4* __restrict__ x, R
   for (int j = 0; j < k; ++j) {
     const int row = __builtin_amdgcn_readlane(my_row, j);
     if (row < 0 || row >= cap) continue;
-    if (on) store_row_policy<kCachePolicySc1Nt>(q, recv + (int64_t)row * nvq, nvq, vq);
+    if (on) store_row_policy<kCachePolicySc1Nt>(q, recv + (int64_t)row * pq, nvq, vq);
     if (scale_lane) recv_scale[(int64_t)row * NB + vq / 8] = s;
   }
 }

@@ -156,7 +156,7 @@ __global__ void __launch_bounds__(kScheduleThreads)
     dispatch_scheduled_kernel(const u32x4* __restrict__ x, const int32_t* __restrict__ send_cnt,
                               const int32_t* __restrict__ seg_off, const int32_t* __restrict__ recv_src,
                               u32x4* __restrict__ recv, float* __restrict__ recv_scale, int R, int E, int rows, int n,
-                              int64_t T, int k, int H, int chunks, int64_t cap) {
+                              int64_t T, int k, int H, int pitch, int chunks, int64_t cap) {
   __shared__ int32_t exp_at[EPL_MAX_EXPERTS];
   __shared__ int32_t cnt_at[EPL_MAX_EXPERTS];
   __shared__ int32_t cum[EPL_MAX_EXPERTS + 1];
@@ -192,9 +192,9 @@ __global__ void __launch_bounds__(kScheduleThreads)
       const int g = src_lds[q];
       if (g < 0 || g >= T) continue;  // only a layout that does not belong to x gets here
       if constexpr (FP8)
-        dispatch_fp8_unit(x, [&] { return row; }, recv, recv_scale, g, u - q * chunks, 1, H, cap, lane);
+        dispatch_fp8_unit(x, [&] { return row; }, recv, recv_scale, g, u - q * chunks, 1, H, pitch / 16, cap, lane);
       else
-        dispatch_bf16_unit<BUF_X>(x, [&] { return row; }, recv, g, u - q * chunks, 1, H / 8, cap, lane);
+        dispatch_bf16_unit<BUF_X>(x, [&] { return row; }, recv, g, u - q * chunks, 1, H / 8, pitch / 8, cap, lane);
     }
     __syncthreads();  // the batch's rows are consumed before the next batch overwrites them
   }
@@ -210,7 +210,7 @@ hipError_t launch_hop_schedule(const int32_t* send_cnt, const int32_t* order, co
 
 hipError_t launch_dispatch_scheduled(const void* x, const int32_t* send_cnt, const int32_t* seg_off,
                                      const int32_t* recv_src, void* recv, float* recv_scale, int R, int E, int rows,
-                                     int n, int64_t T, int k, int H, int64_t cap, hipStream_t stream) {
+                                     int n, int64_t T, int k, int H, int pitch, int64_t cap, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const bool fp8 = recv_scale != nullptr;
   const int chunks = fp8 ? (H + 1023) / 1024 : (H / 8 + kBf16Cols - 1) / kBf16Cols;
@@ -219,13 +219,13 @@ hipError_t launch_dispatch_scheduled(const void* x, const int32_t* send_cnt, con
   u32x4* rv = static_cast<u32x4*>(recv);
   if (fp8)
     hipLaunchKernelGGL((dispatch_scheduled_kernel<false, true>), grid, dim3(kScheduleThreads), 0, stream, xv, send_cnt,
-                       seg_off, recv_src, rv, recv_scale, R, E, rows, n, T, k, H, chunks, cap);
+                       seg_off, recv_src, rv, recv_scale, R, E, rows, n, T, k, H, pitch, chunks, cap);
   else if (T * (int64_t)H * 2 >= kBufferLoadXBytes)
     hipLaunchKernelGGL((dispatch_scheduled_kernel<true, false>), grid, dim3(kScheduleThreads), 0, stream, xv, send_cnt,
-                       seg_off, recv_src, rv, nullptr, R, E, rows, n, T, k, H, chunks, cap);
+                       seg_off, recv_src, rv, nullptr, R, E, rows, n, T, k, H, pitch, chunks, cap);
   else
     hipLaunchKernelGGL((dispatch_scheduled_kernel<false, false>), grid, dim3(kScheduleThreads), 0, stream, xv,
-                       send_cnt, seg_off, recv_src, rv, nullptr, R, E, rows, n, T, k, H, chunks, cap);
+                       send_cnt, seg_off, recv_src, rv, nullptr, R, E, rows, n, T, k, H, pitch, chunks, cap);
   return hipGetLastError();
 }
 

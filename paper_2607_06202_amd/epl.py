@@ -37,21 +37,42 @@ class EplError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [("num_ranks", ctypes.c_int32), ("num_experts", ctypes.c_int32), ("topk", ctypes.c_int32),
-                ("hidden", ctypes.c_int32), ("tokens_per_rank", ctypes.c_int32), ("payload", ctypes.c_int32)]
+                ("hidden", ctypes.c_int32), ("tokens_per_rank", ctypes.c_int32), ("payload", ctypes.c_int32),
+                ("row_pitch", ctypes.c_int32)]
 
     @property
     def T(self) -> int:
         return self.num_ranks * self.tokens_per_rank
 
+    @property
+    def pitch(self) -> int:
+        """Elements from one recv (and y) row to the next."""
+        return self.row_pitch or self.hidden
+
     def __repr__(self) -> str:
-        return "Config(R=%d, E=%d, k=%d, H=%d, Tr=%d, payload=%d)" % (
-            self.num_ranks, self.num_experts, self.topk, self.hidden, self.tokens_per_rank, self.payload)
+        return "Config(R=%d, E=%d, k=%d, H=%d, Tr=%d, payload=%d, row_pitch=%d)" % (
+            self.num_ranks, self.num_experts, self.topk, self.hidden, self.tokens_per_rank, self.payload,
+            self.row_pitch)
 
 
-def config(R: int, E: int, k: int, H: int, Tr: int, payload: str | int = "bf16") -> Config:
+def config(R: int, E: int, k: int, H: int, Tr: int, payload: str | int = "bf16", row_pitch: int = 0) -> Config:
+    """row_pitch: elements from one receive row to the next (0: H, rows packed without gaps)."""
     if isinstance(payload, str):
         payload = {"bf16": PAYLOAD_BF16, "fp8": PAYLOAD_FP8_E4M3}[payload]
-    return Config(R, E, k, H, Tr, payload)
+    return Config(R, E, k, H, Tr, payload, row_pitch)
+
+
+def padded_pitch(H: int, payload: str | int = "bf16") -> int:
+    """The row pitch the benchmark uses. bf16 rows: the smallest multiple of 64 elements at or
+    above H whose byte size is 1.5 KiB past a multiple of 2 KiB (H + 768 for H = 7168, so that
+    consecutive rows do not start 2 KiB-aligned); measured only at H = 7168, where it took 1-4% off
+    the decode-sized layer. fp8 payloads: 0 (packed rows), as padded fp8 rows measured 0.7% slower."""
+    if payload in ("fp8", PAYLOAD_FP8_E4M3):
+        return 0
+    p = (H + 63) // 64 * 64
+    while (2 * p) % 2048 != 1536:
+        p += 64
+    return p
 
 
 class DecomposedOpts(ctypes.Structure):
@@ -236,6 +257,20 @@ def _rows_of(t: torch.Tensor, name: str, width: int) -> int:
     return t.shape[0]
 
 
+def _pitched_rows(t, name: str, dtype, cfg: Config) -> int:
+    """A receive-layout tensor (recv, or y for combine): 2-D [rows, H] on the GPU whose rows are
+    cfg.pitch elements apart (a view of a [rows, pitch] buffer, or contiguous when the pitch is H).
+    Returns its row count."""
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    rows = _rows_of(t, name, cfg.hidden)
+    if (cfg.hidden > 1 and t.stride(1) != 1) or (rows > 1 and t.stride(0) != cfg.pitch):
+        raise ValueError("%s rows must be %d elements apart and dense, got strides %s" % (name, cfg.pitch, t.stride()))
+    return rows
+
+
 def _layout_args(cfg: Config, topk_idx: torch.Tensor, out: Layout | None) -> Layout:
     """Checks shared by the calls that run the layout; returns the Layout to fill."""
     _dev(topk_idx, "topk_idx", torch.int32)
@@ -359,10 +394,12 @@ def alloc_recv(cfg: Config, device, rows: int | None = None, contiguous: bool = 
     rows = max(recv_rows_cap(cfg) if rows is None else rows, 1)
     fp8 = cfg.payload == PAYLOAD_FP8_E4M3
     dtype = torch.uint8 if fp8 else torch.bfloat16
+    P = cfg.pitch
     if contiguous:
-        recv = _ContiguousBlock(rows * cfg.hidden * dtype.itemsize, device).tensor((rows, cfg.hidden), dtype)
+        recv = _ContiguousBlock(rows * P * dtype.itemsize, device).tensor((rows, P), dtype)
     else:
-        recv = torch.empty(rows, cfg.hidden, dtype=dtype, device=device)
+        recv = torch.empty(rows, P, dtype=dtype, device=device)
+    recv = recv[:, :cfg.hidden]  # rows P elements apart (the whole buffer when P == H)
     scale = torch.empty(rows, cfg.hidden // 128, dtype=torch.float32, device=device) if fp8 else None
     return recv, scale
 
@@ -378,8 +415,7 @@ def dispatch(cfg: Config, x: torch.Tensor, L: Layout, recv: torch.Tensor | None 
     if recv is None:
         recv, recv_scale = alloc_recv(cfg, dev)
     fp8 = cfg.payload == PAYLOAD_FP8_E4M3
-    _dev(recv, "recv", torch.uint8 if fp8 else torch.bfloat16)
-    rows = _rows_of(recv, "recv", cfg.hidden)
+    rows = _pitched_rows(recv, "recv", torch.uint8 if fp8 else torch.bfloat16, cfg)
     sp = None
     if fp8:
         sp = _dev(recv_scale, "recv_scale", torch.float32)
@@ -402,8 +438,7 @@ def _recv_args(cfg: Config, x: torch.Tensor, recv, recv_scale, dev):
     if recv is None:
         recv, recv_scale = alloc_recv(cfg, dev)
     fp8 = cfg.payload == PAYLOAD_FP8_E4M3
-    _dev(recv, "recv", torch.uint8 if fp8 else torch.bfloat16)
-    rows = _rows_of(recv, "recv", cfg.hidden)
+    rows = _pitched_rows(recv, "recv", torch.uint8 if fp8 else torch.bfloat16, cfg)
     sp = None
     if fp8:
         sp = _dev(recv_scale, "recv_scale", torch.float32)
@@ -505,10 +540,18 @@ def layer_sentinel(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, topk_w:
 
 
 def sentinel_fill(buf: torch.Tensor) -> torch.Tensor:
-    """epl_sentinel_fill over a whole contiguous bf16 GPU tensor."""
-    _dev(buf, "buf", torch.bfloat16)
+    """epl_sentinel_fill over a bf16 GPU tensor: a contiguous one, or a 2-D view of rows with a
+    pitch (as alloc_recv returns), filled from its first element to its last, the gaps between
+    rows included."""
+    if not isinstance(buf, torch.Tensor) or buf.device.type != "cuda" or buf.dtype != torch.bfloat16:
+        raise ValueError("buf must be a bf16 GPU tensor")
+    if buf.dim() == 2 and buf.shape[0] > 1 and buf.stride(1) == 1 and buf.stride(0) >= buf.shape[1]:
+        n = (buf.shape[0] - 1) * buf.stride(0) + buf.shape[1]
+    else:
+        _dev(buf, "buf", torch.bfloat16)
+        n = buf.numel()
     with _on(buf.device):
-        _check(lib().epl_sentinel_fill(buf.data_ptr(), buf.numel(), _stream(buf.device)), "epl_sentinel_fill")
+        _check(lib().epl_sentinel_fill(buf.data_ptr(), n, _stream(buf.device)), "epl_sentinel_fill")
     return buf
 
 
@@ -615,10 +658,9 @@ def dispatch_scheduled(cfg: Config, x: torch.Tensor, L: Layout, workers: int, re
 
 
 def combine(cfg: Config, y: torch.Tensor, topk_w: torch.Tensor, L: Layout, out: torch.Tensor | None = None):
-    """epl_combine: y [>=P, H] bf16, topk_w [T, k] fp32 -> out [T, H] bf16."""
+    """epl_combine: y [>=P, H] bf16 with rows cfg.pitch apart, topk_w [T, k] fp32 -> out [T, H] bf16."""
     dev = y.device
-    _dev(y, "y", torch.bfloat16)
-    _rows_of(y, "y", cfg.hidden)  # its row count must cover P, which only the device knows
+    _pitched_rows(y, "y", torch.bfloat16, cfg)  # its row count must cover P, which only the device knows
     _dev(topk_w, "topk_w", torch.float32)
     if _rows_of(topk_w, "topk_w", cfg.topk) < cfg.T:
         raise ValueError("topk_w has %d rows, needs T = %d" % (topk_w.shape[0], cfg.T))
@@ -657,8 +699,7 @@ class PreparedLayer:
         for x in xs:
             recv, recv_scale, sp, rows = _recv_args(cfg, x, recv, recv_scale, dev)
         y = recv if y is None else y
-        _dev(y, "y", torch.bfloat16)
-        _rows_of(y, "y", cfg.hidden)
+        _pitched_rows(y, "y", torch.bfloat16, cfg)
         _dev(topk_w, "topk_w", torch.float32)
         if _rows_of(topk_w, "topk_w", cfg.topk) < cfg.T:
             raise ValueError("topk_w has %d rows, needs T = %d" % (topk_w.shape[0], cfg.T))

@@ -77,7 +77,16 @@ bool same(const char* what, const std::vector<T>& got, const std::vector<T>& wan
 struct Case {
   int R, E, k, Tr, H;
   epl_payload payload;
+  int pitch;  // epl_config.row_pitch (0: packed rows)
 };
+
+// Rows 0..P-1 of a [rows][pitch] buffer, without the gaps.
+template <typename T>
+std::vector<T> payload_rows(const std::vector<T>& buf, size_t P, int H, int pitch) {
+  std::vector<T> out(P * H);
+  for (size_t r = 0; r < P; ++r) std::memcpy(&out[r * H], &buf[r * pitch], H * sizeof(T));
+  return out;
+}
 
 // How layout and dispatch are called: epl_layout then epl_dispatch, one epl_layout_dispatch
 // call, or its two phases epl_layout_counts then epl_dispatch_rows.
@@ -96,7 +105,10 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
   std::vector<float> w(Tk);
   for (auto& v : w) v = (float)(splitmix(seed) % 1000) / 1000.0f - 0.25f;
 
-  epl_config cfg{c.R, c.E, c.k, c.H, c.Tr, c.payload};
+  epl_config cfg{c.R, c.E, c.k, c.H, c.Tr, c.payload, c.pitch};
+  const int PP = c.pitch ? c.pitch : c.H;  // elements from one recv (and y) row to the next
+  std::vector<uint16_t> y_pitched((size_t)Tk * PP, 0x7FC3);  // NaN patterns in the gaps
+  for (int64_t r = 0; r < Tk; ++r) std::memcpy(&y_pitched[r * PP], &y[r * c.H], c.H * 2);
   // reference
   std::vector<int32_t> r_send(c.R * c.E), r_rank(c.R * c.R), r_eoff(c.E + 1), r_roff(c.R + 1), r_seg(c.E * c.R),
       r_ntok(T), r_row(Tk), r_slot(Tk), r_src(Tk), r_j(Tk), r_inv(1);
@@ -124,11 +136,11 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
   void* ws = nullptr;
   HIP_OK(hipMalloc(&ws, ws_bytes));
   uint16_t* d_x = dev_copy(x);
-  uint16_t* d_y = dev_copy(y);
+  uint16_t* d_y = dev_copy(y_pitched);
   float* d_w = dev_copy(w);
   void* d_recv = nullptr;
   float* d_scale = nullptr;
-  HIP_OK(hipMalloc(&d_recv, (size_t)std::max<int64_t>(Tk, 1) * c.H * (fp8 ? 1 : 2)));
+  HIP_OK(hipMalloc(&d_recv, (size_t)std::max<int64_t>(Tk, 1) * PP * (fp8 ? 1 : 2)));
   if (fp8) HIP_OK(hipMalloc(&d_scale, (size_t)std::max<int64_t>(Tk, 1) * (c.H / 128) * sizeof(float)));
   uint16_t* d_o = nullptr;
   HIP_OK(hipMalloc(&d_o, (size_t)std::max<int64_t>(T, 1) * c.H * 2));
@@ -156,12 +168,14 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
     std::vector<uint8_t> q((size_t)Tk * c.H);
     std::vector<float> s((size_t)Tk * (c.H / 128));
     eplref_dispatch_fp8(T, c.k, c.H, x.data(), r_row.data(), q.data(), s.data());
-    ok = same("fp8 rows", host_copy((const uint8_t*)d_recv, (size_t)P * c.H), q, (size_t)P * c.H) &&
+    ok = same("fp8 rows", payload_rows(host_copy((const uint8_t*)d_recv, (size_t)P * PP), P, c.H, PP), q,
+              (size_t)P * c.H) &&
          same("fp8 scales", host_copy(d_scale, (size_t)P * (c.H / 128)), s, (size_t)P * (c.H / 128));
   } else if (ok) {
     std::vector<uint16_t> rr((size_t)Tk * c.H);
     eplref_dispatch_bf16(T, c.k, c.H, x.data(), r_row.data(), rr.data());
-    ok = same("bf16 rows", host_copy((const uint16_t*)d_recv, (size_t)P * c.H), rr, (size_t)P * c.H);
+    ok = same("bf16 rows", payload_rows(host_copy((const uint16_t*)d_recv, (size_t)P * PP), P, c.H, PP), rr,
+              (size_t)P * c.H);
   }
   if (ok) {
     std::vector<uint16_t> o((size_t)T * c.H);
@@ -196,7 +210,7 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
     HIP_OK(hipMalloc(&d_so, so.size() * 4));
     HIP_OK(hipMalloc(&d_cnt, cnt.size() * 4));
     void* d_recv2 = nullptr;
-    HIP_OK(hipMalloc(&d_recv2, std::max<size_t>(1, (size_t)Tk * c.H * 2)));
+    HIP_OK(hipMalloc(&d_recv2, std::max<size_t>(1, (size_t)Tk * PP * 2)));
     ok = epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, n, NH, d_se, d_so, d_cnt, stream) == EPL_OK &&
          epl_dispatch_scheduled(&cfg, d_x, &L, d_recv2, nullptr, Tk, 0, n, stream) == EPL_OK;
     HIP_OK(hipStreamSynchronize(stream));
@@ -205,7 +219,8 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
     ok = ok && same("schedule start expert", host_copy(d_se, se.size()), se, se.size()) &&
          same("schedule start offset", host_copy(d_so, so.size()), so, so.size()) &&
          same("schedule class counts", host_copy(d_cnt, cnt.size()), cnt, cnt.size()) &&
-         same("scheduled dispatch rows", host_copy((const uint16_t*)d_recv2, (size_t)P * c.H), rr, (size_t)P * c.H);
+         same("scheduled dispatch rows",
+              payload_rows(host_copy((const uint16_t*)d_recv2, (size_t)P * PP), P, c.H, PP), rr, (size_t)P * c.H);
     ok = ok && epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, 0, NH, d_se, d_so, d_cnt, stream) ==
                    EPL_ERR_INVALID_ARG &&
          epl_hop_schedule(&cfg, d_out[0], nullptr, 0, d_hop, n, EPL_MAX_HOP_CLASSES + 1, d_se, d_so, d_cnt, stream) ==
@@ -223,7 +238,12 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
   if (ok) {
     epl_config bad = cfg;
     bad.num_experts = c.E + 1;
+    epl_config bad_pitch = cfg;
+    bad_pitch.row_pitch = c.H + 32;  // not a multiple of 64
     ok = epl_layout(&bad, d_idx, &L, ws, ws_bytes, stream) == EPL_ERR_INVALID_ARG &&
+         epl_layout_dispatch(&bad_pitch, d_idx, &L, ws, ws_bytes, d_x, d_recv, d_scale, Tk, stream) ==
+             EPL_ERR_INVALID_ARG &&
+         epl_combine(&bad_pitch, d_y, d_w, &L, d_o, stream) == EPL_ERR_INVALID_ARG &&
          epl_layout(&cfg, d_idx, &L, ws, ws_bytes - 4, stream) == EPL_ERR_WORKSPACE &&
          epl_dispatch(&cfg, d_x, &L, d_recv, d_scale, Tk - 1, stream) == EPL_ERR_CAPACITY &&
          epl_dispatch(&cfg, d_x, &L, (char*)d_recv + 2, d_scale, Tk, stream) == EPL_ERR_ALIGN &&
@@ -250,7 +270,7 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
   HIP_OK(hipFree(d_recv));
   if (d_scale) HIP_OK(hipFree(d_scale));
   HIP_OK(hipFree(d_o));
-  std::printf("case R=%d E=%d k=%d Tr=%d H=%d %s %s (%d launches): %s\n", c.R, c.E, c.k, c.Tr, c.H,
+  std::printf("case R=%d E=%d k=%d Tr=%d H=%d pitch=%d %s %s (%d launches): %s\n", c.R, c.E, c.k, c.Tr, c.H, PP,
               fp8 ? "fp8" : "bf16", kModeName[mode],
               mode == kSeparate ? epl_layout_launches(&cfg) + 1 : epl_layout_dispatch_launches(&cfg),
               ok ? "ok" : "FAILED");
@@ -269,6 +289,9 @@ int main() {
       {32, 256, 8, 80, 256, EPL_PAYLOAD_BF16},    // T*k = 20480: three-launch layout
       {64, 256, 8, 40, 1024, EPL_PAYLOAD_BF16},   // finalize fused into the row kernel
       {2, 8, 3, 0, 64, EPL_PAYLOAD_BF16},         // no tokens
+      {64, 256, 8, 40, 1024, EPL_PAYLOAD_BF16, 1024 + 768},  // fused, rows 1.5 KiB apart beyond their 2 KiB
+      {4, 16, 8, 100, 512, EPL_PAYLOAD_FP8_E4M3, 576},       // fp8 rows 64 bytes apart beyond their 512
+      {32, 256, 8, 80, 256, EPL_PAYLOAD_BF16, 320},          // three-launch layout, padded rows
   };
   bool ok = true;
   uint64_t seed = 12345;

@@ -251,29 +251,50 @@ def test_binding_rejects_host_tensors_before_any_call():
 from hypothesis import given, settings, strategies as st  # noqa: E402
 
 
-def _valid(R, E, k, H, Tr, payload):
+def _valid(R, E, k, H, Tr, payload, P=0):
     """The config rules documented in include/epl.h."""
     return (R >= 1 and R <= E <= epl.MAX_EXPERTS and E % R == 0 and 1 <= k <= 32 and Tr >= 0 and 8 <= H <= 1 << 20
-            and H % 8 == 0 and R * Tr * k < 2 ** 31 - 1 and payload in (0, 1))
+            and H % 8 == 0 and R * Tr * k < 2 ** 31 - 1 and payload in (0, 1)
+            and (P == 0 or (H <= P <= 1 << 20 and P % 64 == 0)))
 
 
 @settings(max_examples=400, deadline=None)
 @given(R=st.one_of(st.integers(-2, 70), st.sampled_from([128, 256, 1024, 1025])),
        E=st.one_of(st.integers(-2, 300), st.sampled_from([512, 1024, 1025, 2048])),
        k=st.integers(-1, 34), H=st.one_of(st.integers(-8, 300), st.sampled_from([7168, 1 << 20, (1 << 20) + 8])),
-       Tr=st.one_of(st.integers(-2, 5000), st.sampled_from([1 << 20, 1 << 24])), payload=st.integers(-1, 2))
-def test_config_rules_property(lib, R, E, k, H, Tr, payload):
-    """Host-side validation follows the documented rules for any config; rejected configs never
-    reach a launch (the calls below use fake pointers and would fault if they did)."""
-    c = epl.Config(R, E, k, H, Tr, payload)
-    ok = _valid(R, E, k, H, Tr, payload)
+       Tr=st.one_of(st.integers(-2, 5000), st.sampled_from([1 << 20, 1 << 24])), payload=st.integers(-1, 2),
+       P=st.one_of(st.just(0), st.integers(-70, 400),
+                   st.sampled_from([7168, 7168 + 768, 7168 + 8, 7104, 1 << 20, (1 << 20) + 64])))
+def test_config_rules_property(lib, R, E, k, H, Tr, payload, P):
+    """Host-side validation follows the documented rules for any config, row pitch included;
+    rejected configs never reach a launch (the calls below use fake pointers and would fault if
+    they did)."""
+    c = epl.Config(R, E, k, H, Tr, payload, P)
+    ok = _valid(R, E, k, H, Tr, payload, P)
     assert (lib.epl_workspace_bytes(ctypes.byref(c)) > 0) == ok
     n = lib.epl_layout_launches(ctypes.byref(c))
     assert (n in (1, 3)) if ok else n == -1
     if not ok:
         st_ = call_layout(lib, c)
         assert st_ in (INVALID, UNSUPPORTED)
-        assert (st_ == UNSUPPORTED) == (payload not in (0, 1) and _valid(R, E, k, H, Tr, 0))
+        assert (st_ == UNSUPPORTED) == (payload not in (0, 1) and _valid(R, E, k, H, Tr, 0, P))
+
+
+def test_row_pitch_rule_and_padded_pitch(lib):
+    """The pitch rule at its edges, for every call that takes a config, and the benchmark's padded
+    pitch: a multiple of 64 elements at or above H whose rows are 1.5 KiB past a 2 KiB multiple."""
+    for P, ok in ((0, True), (7168, True), (7168 + 64, True), (7168 + 768, True), (1 << 20, True),
+                  (7104, False), (7168 + 8, False), (7168 + 32, False), (-64, False), ((1 << 20) + 64, False)):
+        for payload in (0, 1):
+            c = epl.Config(64, 256, 8, 7168, 128, payload, P)
+            assert (lib.epl_workspace_bytes(ctypes.byref(c)) > 0) == ok, (P, payload)
+            if not ok:
+                assert call_layout(lib, c) == INVALID
+    assert epl.padded_pitch(7168) == 7168 + 768 and epl.padded_pitch(7168, "fp8") == 0
+    for H in range(8, 20000, 8):
+        p = epl.padded_pitch(H)
+        assert p >= H and p % 64 == 0 and (2 * p) % 2048 == 1536 and p - H < 1024 + 64
+    assert epl.config(2, 4, 1, 64, 3).pitch == 64 and epl.config(2, 4, 1, 64, 3, row_pitch=128).pitch == 128
 
 
 def test_contiguous_block_views_must_fit_the_block():

@@ -2,7 +2,8 @@
 
 The benchmark's layer is epl_layout_dispatch (the layout's counts, then the row kernel, with the
 finalize step fused in where it applies) into a receive buffer allocated as one physically
-contiguous block, then epl_combine reading that buffer (identity experts). These tests run
+contiguous block at the benchmark's row pitch, then epl_combine reading that buffer (identity
+experts). These tests run
 exactly that sequence, at the named workloads' full sizes, after a first layer with other
 routing has left its data in every buffer, and compare with the CPU oracle:
 * every layout output;
@@ -35,6 +36,18 @@ def _recv(cfg, dev):
         return epl.alloc_recv(cfg, dev)
 
 
+def _bench_cfg(w):
+    """The benchmark's config of a workload: its default row pitch included."""
+    return epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload, row_pitch=epl.padded_pitch(w.H, w.payload))
+
+
+def _pitched_like(cfg, y):
+    """y [P, H] copied into rows cfg.pitch apart (the gaps hold NaN patterns)."""
+    blk = torch.full((y.shape[0], cfg.pitch), 0x7FC3, dtype=torch.int16, device=y.device).view(torch.bfloat16)
+    blk[:, :cfg.hidden].copy_(y)
+    return blk[:, :cfg.hidden]
+
+
 def _bench_layer(cfg, idx_d, x_d, w_d, L, recv, scale, y, out):
     """One step as bench.py issues it: epl_layout_dispatch, then epl_combine."""
     epl.layout_dispatch(cfg, idx_d, x_d, out=L, recv=recv, recv_scale=scale)
@@ -57,7 +70,8 @@ def test_bench_layer_full_size_every_element(name):
     dev = device()
     w = W.WORKLOADS[name]
     fp8 = w.payload == "fp8"
-    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)
+    cfg = _bench_cfg(w)
+    assert cfg.pitch == (w.H if fp8 else w.H + 768)
     x = W.tokens_bf16(w)
     x_d = to_dev_bf16(x, dev)
     gw = W.gate_weights(w)
@@ -65,7 +79,7 @@ def test_bench_layer_full_size_every_element(name):
     L = epl.alloc_layout(cfg, dev)
     recv, scale = _recv(cfg, dev)
     out = torch.empty(w.T, w.H, dtype=torch.bfloat16, device=dev)
-    y_zero = torch.zeros(epl.recv_rows_cap(cfg), w.H, dtype=torch.bfloat16, device=dev) if fp8 else None
+    y_zero = torch.zeros(epl.recv_rows_cap(cfg), cfg.pitch, dtype=torch.bfloat16, device=dev)[:, :w.H] if fp8 else None
     # a first layer with other routing leaves its rows, metadata and output behind
     idx1 = W.routing(w, 1)
     _bench_layer(cfg, torch.from_numpy(idx1).to(dev), x_d, w_d, L, recv, scale, y_zero if fp8 else recv, out)
@@ -95,7 +109,7 @@ def test_bench_layer_full_size_every_element(name):
         assert torch.equal(out.float(), x_d.float())  # and that is x back (numerically: -0 == +0)
     # combine of independent expert rows through the same buffers
     y_d = W.device_normal_bf16((P, w.H), seed=11, device=dev)
-    epl.combine(cfg, y_d, w_d, L, out)
+    epl.combine(cfg, _pitched_like(cfg, y_d), w_d, L, out)
     torch.cuda.synchronize()
     want = oracle_combine_threaded(bf16_bits(y_d), gw, ref.pair_row)
     np.testing.assert_array_equal(bf16_bits(out), want, err_msg=name + ": combine of independent rows")
@@ -109,7 +123,7 @@ def test_bench_layer_prefill_streamed():
     rows are gathered on the device and copied to the host."""
     dev = device()
     w = W.WORKLOADS["prefill_ep32"]
-    cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload)
+    cfg = _bench_cfg(w)
     idx = W.routing(w)
     idx_d = torch.from_numpy(idx).to(dev)
     x_d = W.device_normal_bf16((w.T, w.H), seed=1, device=dev)
@@ -125,7 +139,7 @@ def test_bench_layer_prefill_streamed():
     assert_layout_equal(L, ref, "prefill")
     _rows_equal_on_device(recv[:P], x_d, ref.recv_src, "prefill")
     y_d = W.device_normal_bf16((P, w.H), seed=12, device=dev)
-    out2 = epl.combine(cfg, y_d, w_d, L)
+    out2 = epl.combine(epl.config(w.R, w.E, w.k, w.H, w.Tr), y_d, w_d, L)  # packed independent rows
     torch.cuda.synchronize()
     chunk = 8192
     for g0 in range(0, w.T, chunk):
