@@ -418,8 +418,9 @@ def main():
     ap.add_argument("--recv-alloc", choices=["contiguous", "torch"], default="contiguous",
                     help="receive buffer: one physically contiguous HIP block (default) or torch's allocator")
     ap.add_argument("--row-pitch", default="auto",
-                    help="elements from one receive row to the next: 'auto' (the library's padded pitch: H + 768 "
-                         "for bf16 rows of 7168, packed rows for fp8), 0 (packed, H) or a multiple of 64 >= H")
+                    help="elements from one receive row to the next: 'auto' (the measured pitch of the binding's "
+                         "TUNED_PITCH table: 7936 for bf16 rows of 7168, else packed), 0 (packed, H) or a multiple "
+                         "of 64 >= H")
     ap.add_argument("--warm", action="store_true",
                     help="read the same x every step (it may stay in the memory-side cache) instead of rotating copies")
     ap.add_argument("--calibrate-copy", action="store_true", help="time a plain 1 GiB device copy instead")
@@ -483,7 +484,7 @@ def main():
     idx = W.routing(w, args.seed)
     x = W.tokens_bf16(w, args.seed)
     gw = W.gate_weights(w, args.seed)
-    pitch = epl.padded_pitch(w.H, w.payload) if args.row_pitch == "auto" else int(args.row_pitch)
+    pitch = epl.tuned_pitch(w.H, w.payload) if args.row_pitch == "auto" else int(args.row_pitch)
     cfg = epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload, row_pitch=pitch)
 
     idx_d = torch.from_numpy(idx).to(dev)

@@ -25,10 +25,11 @@
  *   - So rows run in (destination rank, expert, source rank, token, j) order, with no gaps.
  *   - Row r of recv, and of the expert outputs y that combine reads, starts at element r*pitch,
  *     where pitch = row_pitch, or H when row_pitch is 0. Elements [H, pitch) of a row are never
- *     read or written. A pitch a little above H can be faster than H itself: on MI355X, with
- *     H = 7168 bf16 (14 KiB rows), a pitch of H + 768 (15.5 KiB) took 1-4% off the layer at 64
- *     ranks and 8192 tokens and changed nothing measurable at larger sizes, while H + 1024
- *     (16 KiB, a power of two) made it 2% slower.
+ *     read or written. The pitch moves the time in ways that depend on the row size, so it is a
+ *     value to measure, not a rule: on MI355X, with H = 7168 bf16 (14 KiB rows), H + 768
+ *     (15.5 KiB) took 0.6-4% off the layer at 64 ranks and 8192 tokens and changed nothing
+ *     measurable at larger sizes, H + 1024 (16 KiB) made it 4% slower, and at H = 5120 every
+ *     pitch above H that was tried was slower, by up to 9%.
  *
  * Conventions:
  *   - Every pointer argument is a DEVICE pointer unless stated. The caller allocates and owns

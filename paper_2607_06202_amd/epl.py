@@ -62,17 +62,22 @@ def config(R: int, E: int, k: int, H: int, Tr: int, payload: str | int = "bf16",
     return Config(R, E, k, H, Tr, payload, row_pitch)
 
 
-def padded_pitch(H: int, payload: str | int = "bf16") -> int:
-    """The row pitch the benchmark uses. bf16 rows: the smallest multiple of 64 elements at or
-    above H whose byte size is 1.5 KiB past a multiple of 2 KiB (H + 768 for H = 7168, so that
-    consecutive rows do not start 2 KiB-aligned); measured only at H = 7168, where it took 1-4% off
-    the decode-sized layer. fp8 payloads: 0 (packed rows), as padded fp8 rows measured 0.7% slower."""
-    if payload in ("fp8", PAYLOAD_FP8_E4M3):
-        return 0
-    p = (H + 63) // 64 * 64
-    while (2 * p) % 2048 != 1536:
-        p += 64
-    return p
+# Row pitches measured faster than packed rows on MI355X, by (H, payload); other shapes keep packed
+# rows. Whole layer, one box, 200 steps per pitch (us per layer):
+# * H = 7168 bf16, EP=64 decode: 7168 376.7-377.3, 7424 377.1, 7680 375.1, 7936 373.8, 8192 392.0,
+#   8448 374.5, 9216 381.4 (on other boxes 7936 gained 0.6-3.6%); EP=256, prefill and the DeepSeek
+#   shape neutral (within 0.3%);
+# * H = 5120 bf16 (GLM-4.7 shape): 5120 131.8-132.2, 5248 131.6, 5632 134.5, 5888 144.5, 8192 141.9;
+# * H = 2048 bf16 (Qwen3-30B shape): 39.5-40.1 at every pitch (bound by launches);
+# * H = 7168 fp8: a pitch of 7936 bytes 0.3-0.7% slower.
+TUNED_PITCH = {(7168, PAYLOAD_BF16): 7936}
+
+
+def tuned_pitch(H: int, payload: str | int = "bf16") -> int:
+    """The row pitch the benchmark uses: a measured entry of TUNED_PITCH, else 0 (packed rows)."""
+    if isinstance(payload, str):
+        payload = {"bf16": PAYLOAD_BF16, "fp8": PAYLOAD_FP8_E4M3}[payload]
+    return TUNED_PITCH.get((H, payload), 0)
 
 
 class DecomposedOpts(ctypes.Structure):

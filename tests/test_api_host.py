@@ -280,9 +280,9 @@ def test_config_rules_property(lib, R, E, k, H, Tr, payload, P):
         assert (st_ == UNSUPPORTED) == (payload not in (0, 1) and _valid(R, E, k, H, Tr, 0, P))
 
 
-def test_row_pitch_rule_and_padded_pitch(lib):
-    """The pitch rule at its edges, for every call that takes a config, and the benchmark's padded
-    pitch: a multiple of 64 elements at or above H whose rows are 1.5 KiB past a 2 KiB multiple."""
+def test_row_pitch_rule_and_tuned_pitch(lib):
+    """The pitch rule at its edges, for every call that takes a config, and the benchmark's tuned
+    pitches: valid pitches, and packed rows for every shape without a measured entry."""
     for P, ok in ((0, True), (7168, True), (7168 + 64, True), (7168 + 768, True), (1 << 20, True),
                   (7104, False), (7168 + 8, False), (7168 + 32, False), (-64, False), ((1 << 20) + 64, False)):
         for payload in (0, 1):
@@ -290,10 +290,11 @@ def test_row_pitch_rule_and_padded_pitch(lib):
             assert (lib.epl_workspace_bytes(ctypes.byref(c)) > 0) == ok, (P, payload)
             if not ok:
                 assert call_layout(lib, c) == INVALID
-    assert epl.padded_pitch(7168) == 7168 + 768 and epl.padded_pitch(7168, "fp8") == 0
-    for H in range(8, 20000, 8):
-        p = epl.padded_pitch(H)
-        assert p >= H and p % 64 == 0 and (2 * p) % 2048 == 1536 and p - H < 1024 + 64
+    assert epl.tuned_pitch(7168) == 7936 and epl.tuned_pitch(7168, "fp8") == 0
+    assert epl.tuned_pitch(5120) == 0 and epl.tuned_pitch(2048) == 0 and epl.tuned_pitch(256) == 0
+    for (H, payload), P in epl.TUNED_PITCH.items():
+        c = epl.Config(64, 256, 8, H, 128, payload, P)
+        assert lib.epl_workspace_bytes(ctypes.byref(c)) > 0
     assert epl.config(2, 4, 1, 64, 3).pitch == 64 and epl.config(2, 4, 1, 64, 3, row_pitch=128).pitch == 128
 
 

@@ -37,8 +37,8 @@ def _recv(cfg, dev):
 
 
 def _bench_cfg(w):
-    """The benchmark's config of a workload: its default row pitch included."""
-    return epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload, row_pitch=epl.padded_pitch(w.H, w.payload))
+    """The benchmark's config of a workload: its default (tuned) row pitch included."""
+    return epl.config(w.R, w.E, w.k, w.H, w.Tr, w.payload, row_pitch=epl.tuned_pitch(w.H, w.payload))
 
 
 def _pitched_like(cfg, y):
