@@ -391,7 +391,8 @@ class _ContiguousBlock:
 
 def alloc_recv(cfg: Config, device, rows: int | None = None, contiguous: bool = False):
     """Receive buffer for dispatch: (recv [rows, H] bf16 | uint8, recv_scale [rows, H/128] fp32 |
-    None), rows = T*k by default. With contiguous=True the payload rows are one physically
+    None), rows = T*k by default. recv is a view of a [rows, cfg.pitch] buffer, so its rows are
+    cfg.pitch elements apart as the kernels expect (the whole buffer for packed rows). With contiguous=True the payload rows are one physically
     contiguous block from the HIP runtime instead of torch's allocator (MemoryError if the driver
     has no such block free). The rows are written in a scatter and gathered at random, and where
     they sit in HBM moves both kernels' times: on MI355X, decode-sized layers measured 377.0 us per
