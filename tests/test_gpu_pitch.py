@@ -222,3 +222,52 @@ def test_pitch_mismatch_is_refused_before_any_launch():
         epl.combine(cfg, dense, torch.zeros(512, 2, device=dev), L)
     with pytest.raises(epl.EplError):
         epl.layout(epl.config(4, 16, 2, 256, 128, row_pitch=300), idx_d)
+
+
+def _random_pitched_case(seed):
+    rng = np.random.default_rng(9000 + seed)
+    fp8 = seed % 3 == 2
+    R = int(rng.choice([1, 2, 3, 8, 16, 64]))
+    El = int(rng.integers(1, 5))
+    E = R * El
+    k = int(rng.integers(1, 9))
+    Tr = 0 if seed % 6 == 0 else int(rng.integers(1, 300))
+    H = 128 * int(rng.integers(1, 40)) if fp8 else 8 * int(rng.integers(1, 300))
+    pitch = (H + 63) // 64 * 64 + 64 * int(rng.integers(0, 40))
+    return R, E, k, Tr, H, pitch, "fp8" if fp8 else "bf16"
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shapes_and_pitches(seed):
+    """Random shapes (no tokens, a single rank, ragged rows) at random valid pitches: layout and
+    dispatch in one call, then combine, against the oracle, with the canary checks."""
+    dev = device()
+    R, E, k, Tr, H, pitch, payload = _random_pitched_case(seed)
+    fp8 = payload == "fp8"
+    T = R * Tr
+    idx, x = _case(R, E, k, Tr, H, seed)
+    cfg = epl.config(R, E, k, H, Tr, payload, row_pitch=pitch)
+    ref = oracle.layout(R, E, k, Tr, idx)
+    P = ref.P
+    rows = max(T * k, 1)
+    blk, recv = _block(rows, H, pitch, fp8, dev)
+    sc = torch.full((rows, H // 128), float("nan"), device=dev) if fp8 else None
+    L, _, _ = epl.layout_dispatch(cfg, torch.from_numpy(idx).to(dev), to_dev_bf16(x, dev), recv=recv,
+                                  recv_scale=sc)
+    torch.cuda.synchronize()
+    what = "seed %d: R=%d E=%d k=%d Tr=%d H=%d pitch=%d %s" % (seed, R, E, k, Tr, H, pitch, payload)
+    assert_layout_equal(L, ref, what)
+    if fp8:
+        want_rows, want_scale = oracle.dispatch_fp8(x, ref.pair_row, P)
+        np.testing.assert_array_equal(sc[:P].cpu().numpy().view(np.uint32), want_scale.view(np.uint32))
+    else:
+        want_rows = oracle.dispatch_bf16(x, ref.pair_row, P)
+    _check_block(blk, H, P, want_rows, fp8, what)
+    gw = W.softmax_gate_weights(seed, max(T, 1), k)[:T]
+    y, yh = _pitched_y(max(P, 1), H, pitch, seed, dev)
+    out = epl.combine(cfg, y, torch.from_numpy(np.ascontiguousarray(gw)).to(dev) if T else
+                      torch.zeros(1, k, device=dev), L)
+    torch.cuda.synchronize()
+    if T:
+        np.testing.assert_array_equal(bf16_bits(out[:T]), oracle_combine_threaded(yh, gw, ref.pair_row),
+                                      err_msg=what + " combine")
