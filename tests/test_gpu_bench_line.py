@@ -24,6 +24,7 @@ def test_bench_json_line():
         assert key in d, key
     assert d["n_gpus"] == 1 and d["steps"] == 20 and d["warmup"] == 3
     assert d["config"]["workload"] == "tiny" and d["dtype"] == "bf16" and d["data"] == "synthetic"
+    assert d["config"]["row_pitch"] == d["config"]["hidden"] == 256  # no tuned pitch for 256-wide rows: packed
     assert d["value"] > 0 and d["ms_per_step"] > 0 and d["higher_is_better"] is True
     roof = d["roofline"]
     assert roof["bound"] == "hbm" and roof["peak"] == 8000.0 and roof["unit"] == "GB/s"
