@@ -616,7 +616,7 @@ def main():
             ev[3].record(stream)
 
     def timed_events(n):
-        return [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
+        return [[FenceFreeEvent(epl) for _ in range(4)] for _ in range(n)]
 
     def per_call_us(evs):
         return np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])] for e in evs]) * 1e3
