@@ -255,6 +255,40 @@ epl_status epl_sentinel_fill(void *buf, int64_t n, void *stream);
  * EPL_SENTINEL_BF16, or -1 if none (or values is NULL or n <= 0). No HIP calls.                */
 int64_t epl_sentinel_find(const uint16_t *values, int64_t n);
 
+/* The paper's other two Data-as-Flag variants (Data-as-Flag Synchronization: Token-Flag Fusion
+ * and Data-for-Checksum), as alternatives to Sentinel Polling in the one-launch layer: layout,
+ * dispatch and the combine of the dispatched rows (identity experts) in one launch, the combine
+ * synchronised with the dispatch per 1 KiB chunk of a row. MI355X gives no 512-byte store
+ * atomicity, so neither variant fuses its flag into the payload block:
+ *   EPL_DAF_TOKEN_FLAG_FUSION  a send wave waits for its own row stores to complete, then stores
+ *              `epoch` into the mark of every chunk it wrote; a combine wave polls the chunk's mark
+ *              until it equals `epoch`, then loads the chunk.
+ *   EPL_DAF_DATA_CHECKSUM      a send wave stores, with no wait, a 64-bit hash of each chunk it
+ *              wrote, salted with `epoch`; a combine wave loads the chunk and its mark until the
+ *              salted hash of what it loaded equals the mark. Stale or partly written data fail
+ *              the comparison except with probability about 2^-64.
+ *   marks      [recv_rows_cap * ceil(H/512)] uint64 device, 8-byte aligned: one word per (packed
+ *              row, 1 KiB column chunk); epl_layer_marks_bytes gives its size. Its contents carry
+ *              over from call to call. For EPL_DAF_TOKEN_FLAG_FUSION it must be zero-filled before
+ *              the first call and every call must use an epoch no earlier call on it used; for
+ *              EPL_DAF_DATA_CHECKSUM any contents will do, and each call's epoch must differ from
+ *              the previous one's.
+ *   epoch      nonzero (INVALID_ARG for 0).
+ *   recv       receive rows as epl_layer_sentinel, with no sentinel and no fill: any contents.
+ * Other arguments, outputs and statuses as epl_layer_sentinel; an unknown variant is
+ * INVALID_ARG.                                                                                 */
+#define EPL_DAF_TOKEN_FLAG_FUSION 1
+#define EPL_DAF_DATA_CHECKSUM 2
+epl_status epl_layer_data_as_flag(const epl_config *cfg, const int32_t *topk_idx, const epl_layout_buffers *L,
+                                  void *workspace, size_t workspace_bytes, const void *x, void *recv,
+                                  int64_t recv_rows_cap, const float *topk_w, void *out, uint64_t *marks,
+                                  int32_t variant, uint64_t epoch, const epl_decomposed_opts *opts,
+                                  int32_t *wait_status, void *stream);
+
+/* Bytes of the marks buffer of epl_layer_data_as_flag for recv_rows_cap receive rows; -1 for an
+ * invalid cfg or a negative count. Host-only, no HIP calls.                                    */
+int64_t epl_layer_marks_bytes(const epl_config *cfg, int64_t recv_rows_cap);
+
 /* epl_layout_dispatch without a caller workspace, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc). Same
  * outputs, arguments, statuses and kernels as epl_layout_dispatch, except that the layout's

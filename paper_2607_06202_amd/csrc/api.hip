@@ -239,7 +239,7 @@ EPL_EXPORT epl_status epl_layout_dispatch_decomposed(const epl_config* cfg, cons
   if (!aligned(wait_status, 4)) return EPL_ERR_ALIGN;
   const epl::Geom g = make_geom(cfg);
   epl::DecomposedPlan plan;
-  if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, false, &plan) != hipSuccess) return EPL_ERR_DEVICE;
+  if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, epl::kDafNone, &plan) != hipSuccess) return EPL_ERR_DEVICE;
   if (plan.grid > plan.capacity) return EPL_ERR_UNSUPPORTED;
   return from_hip(epl::launch_decomposed(g, topk_idx, static_cast<int32_t*>(workspace), *L, x, recv, cfg->hidden,
                                          pitch_of(cfg), recv_rows_cap, o, wait_status,
@@ -250,16 +250,20 @@ EPL_EXPORT int epl_decomposed_plan(const epl_config* cfg, int32_t count_groups, 
   if (check_config(cfg) != EPL_OK || count_groups < 0) return -1;
   if (cfg->payload != EPL_PAYLOAD_BF16 || !epl::fused_dispatch_ok(make_geom(cfg), false)) return -1;
   epl::DecomposedPlan plan;
-  if (epl::plan_decomposed(make_geom(cfg), cfg->hidden, count_groups, false, &plan) != hipSuccess) return -1;
+  if (epl::plan_decomposed(make_geom(cfg), cfg->hidden, count_groups, epl::kDafNone, &plan) != hipSuccess) return -1;
   if (grid) *grid = plan.grid;
   if (capacity) *capacity = plan.capacity;
   return plan.count_groups;
 }
 
-EPL_EXPORT epl_status epl_layer_sentinel(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
-                                         void* workspace, size_t ws_bytes, const void* x, void* recv,
-                                         int64_t recv_rows_cap, const float* topk_w, void* out,
-                                         const epl_decomposed_opts* opts, int32_t* wait_status, void* stream) {
+namespace {
+
+// The checks and the launch shared by the one-launch layer calls (Sentinel Polling, and the
+// flag and checksum variants).
+epl_status run_layer(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L, void* workspace,
+                     size_t ws_bytes, const void* x, void* recv, int64_t recv_rows_cap, const float* topk_w, void* out,
+                     const epl_decomposed_opts* opts, int32_t* wait_status, void* stream, int sync, uint64_t* marks,
+                     uint64_t epoch) {
   epl_status st = check_layout_dispatch(cfg, topk_idx, L, workspace, ws_bytes, x, recv, nullptr, recv_rows_cap);
   if (st != EPL_OK) return st;
   epl::DecomposedOpts o;
@@ -268,12 +272,49 @@ EPL_EXPORT epl_status epl_layer_sentinel(const epl_config* cfg, const int32_t* t
   if (g.T > 0 && (!topk_w || !out)) return EPL_ERR_INVALID_ARG;
   if (!wait_status) return EPL_ERR_INVALID_ARG;
   if (!aligned(wait_status, 4) || !aligned(topk_w, 4) || !aligned(out, 16)) return EPL_ERR_ALIGN;
+  if (sync != epl::kDafSentinel) {
+    if (g.T > 0 && !marks) return EPL_ERR_INVALID_ARG;
+    if (!aligned(marks, 8)) return EPL_ERR_ALIGN;
+    if (epoch == 0) return EPL_ERR_INVALID_ARG;
+  }
   epl::DecomposedPlan plan;
-  if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, true, &plan) != hipSuccess) return EPL_ERR_DEVICE;
+  if (epl::plan_decomposed(g, cfg->hidden, o.count_groups, sync, &plan) != hipSuccess) return EPL_ERR_DEVICE;
   if (plan.grid > plan.capacity) return EPL_ERR_UNSUPPORTED;
   return from_hip(epl::launch_decomposed(g, topk_idx, static_cast<int32_t*>(workspace), *L, x, recv, cfg->hidden,
                                          pitch_of(cfg), recv_rows_cap, o, wait_status,
-                                         static_cast<hipStream_t>(stream), topk_w, out));
+                                         static_cast<hipStream_t>(stream), sync, topk_w, out, marks, epoch));
+}
+
+}  // namespace
+
+EPL_EXPORT epl_status epl_layer_sentinel(const epl_config* cfg, const int32_t* topk_idx, const epl_layout_buffers* L,
+                                         void* workspace, size_t ws_bytes, const void* x, void* recv,
+                                         int64_t recv_rows_cap, const float* topk_w, void* out,
+                                         const epl_decomposed_opts* opts, int32_t* wait_status, void* stream) {
+  return run_layer(cfg, topk_idx, L, workspace, ws_bytes, x, recv, recv_rows_cap, topk_w, out, opts, wait_status,
+                   stream, epl::kDafSentinel, nullptr, 0);
+}
+
+EPL_EXPORT int64_t epl_layer_marks_bytes(const epl_config* cfg, int64_t recv_rows_cap) {
+  if (check_config(cfg) != EPL_OK || recv_rows_cap < 0) return -1;
+  const int64_t cchunks = (cfg->hidden / 8 + 63) / 64;
+  return recv_rows_cap * cchunks * (int64_t)sizeof(uint64_t);
+}
+
+EPL_EXPORT epl_status epl_layer_data_as_flag(const epl_config* cfg, const int32_t* topk_idx,
+                                             const epl_layout_buffers* L, void* workspace, size_t ws_bytes,
+                                             const void* x, void* recv, int64_t recv_rows_cap, const float* topk_w,
+                                             void* out, uint64_t* marks, int32_t variant, uint64_t epoch,
+                                             const epl_decomposed_opts* opts, int32_t* wait_status, void* stream) {
+  int sync;
+  if (variant == EPL_DAF_TOKEN_FLAG_FUSION)
+    sync = epl::kDafFlag;
+  else if (variant == EPL_DAF_DATA_CHECKSUM)
+    sync = epl::kDafChecksum;
+  else
+    return check_config(cfg) != EPL_OK ? check_config(cfg) : EPL_ERR_INVALID_ARG;
+  return run_layer(cfg, topk_idx, L, workspace, ws_bytes, x, recv, recv_rows_cap, topk_w, out, opts, wait_status,
+                   stream, sync, marks, epoch);
 }
 
 EPL_EXPORT epl_status epl_sentinel_fill(void* buf, int64_t n, void* stream) {

@@ -59,8 +59,10 @@ struct DecomposedArgs {
   int32_t* seg_rel;
   int32_t* num_invalid;
   int32_t* cnt;                // [nblk][E] chunk-major expert counts
-  const float* topk_w;         // the combine role (the layer with Sentinel Polling): [T*k] weights
+  const float* topk_w;         // the combine role (the layer variants): [T*k] weights
   u32x4* out;                  // [T][H] bf16
+  uint64_t* marks;             // Token-Flag Fusion and Data-for-Checksum: [cap][cchunks] words, one per 1 KiB
+  uint64_t epoch;              // this call's epoch: the flag value, or the checksum's salt
   int cchunks, nco;            // 1 KiB column chunks per row; combine workgroups
   const u32x4* x;
   u32x4* recv;
@@ -145,7 +147,11 @@ __device__ __forceinline__ bool holds_sentinel(u32x4 v);
 // Measured against handing out batches of units from a launch-wide counter, with the count
 // workgroups joining once their counting was done: that was slower (decode 416.7 against
 // 396.8 us per layer, the Qwen3-30B shape 61.2 against 50.7 us), the counter's atomics serialising.
-template <bool BUF_X, bool LAYER>
+template <int SYNC>
+__device__ __forceinline__ void publish_marks(const DecomposedArgs& A, const u32x4* buf, const bool* on, int my_row,
+                                              int c, int k, int lane);
+
+template <bool BUF_X, int SYNC>
 __device__ __forceinline__ void send_role(const DecomposedArgs& A, int j, int32_t* lds, int32_t* flag) {
   const int lane = threadIdx.x % kWave;
   const int w = threadIdx.x / kWave;
@@ -182,13 +188,17 @@ __device__ __forceinline__ void send_role(const DecomposedArgs& A, int j, int32_
           __syncthreads();  // every wave has its rows before the next iteration rewrites them
           return r;
         },
-        A.recv, g, c, k, A.nv, A.pv, A.cap, lane, active, [&](const u32x4* buf, const bool* on) {
-          if constexpr (LAYER) {
+        A.recv, g, c, k, A.nv, A.pv, A.cap, lane, active,
+        [&](const u32x4* buf, const bool* on) {
+          if constexpr (SYNC == kDafSentinel) {
             bool seen = false;
 #pragma unroll
             for (int q = 0; q < kBf16VPL; ++q) seen |= on[q] && holds_sentinel(buf[q]);
             if (__ballot(seen) != 0 && lane == 0) atomicOr(&A.sync[kSyncStatus], kSentinelInX);
           }
+        },
+        [&](const u32x4* buf, const bool* on, int my_row) {
+          if constexpr (SYNC == kDafFlag || SYNC == kDafChecksum) publish_marks<SYNC>(A, buf, on, my_row, c, k, lane);
         });
   }
 }
@@ -235,10 +245,122 @@ __device__ __forceinline__ bool poll_vec(const u32x4* row, int nv, int v, u32x4&
   }
 }
 
+// ------------------------------------------------------------------------ Token-Flag Fusion, Data-for-Checksum
+// The paper's other two Data-as-Flag variants, for a GPU without multi-word store atomicity. Both
+// keep one 64-bit word per (packed row, 1 KiB column chunk) in `marks`, beside the rows, and an
+// epoch that the caller changes on every call, so nothing has to be reset between layers.
+// * Token-Flag Fusion: the paper stores a flag field and the payload in one atomic 512-byte block.
+//   Here a send wave waits until its own device-scope row stores are complete (vmcnt), then stores
+//   the epoch into the marks of the chunks it wrote; a combine wave polls the mark until it holds
+//   the epoch and only then loads the chunk. The wait on the sender is what the fused flag avoids
+//   on the paper's fabric.
+// * Data-for-Checksum: the paper's receiver waits for a checksum of the batch's leading markers,
+//   written after the batch. Without block atomicity a marker does not vouch for the rest of its
+//   block, so the checksum here covers every byte of its 1 KiB chunk: a 64-bit hash of the chunk,
+//   salted with the epoch. The send wave stores it with no wait at all; a combine wave loads the
+//   chunk and the mark and accepts the chunk when the hash of what it loaded, salted the same way,
+//   equals the mark (else it loads both again). Stale data, a stale mark, or a chunk only partly
+//   written all fail the comparison except with probability about 2^-64.
+__device__ __forceinline__ uint64_t ld64_dev(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st64_dev(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The SplitMix64 output function (Steele, Lea and Flood, "Fast splittable pseudorandom number
+// generators", OOPSLA 2014): a bijective 64-bit mixer.
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// One lane's 16 bytes at lane position `lane` of its chunk, mixed; lanes outside the row give 0.
+__device__ __forceinline__ uint64_t lane_hash(u32x4 v, bool on, int lane) {
+  const uint64_t a = (uint64_t)v[0] | ((uint64_t)v[1] << 32);
+  const uint64_t b = (uint64_t)v[2] | ((uint64_t)v[3] << 32);
+  return on ? mix64(a ^ mix64(b + 0x9E3779B97F4A7C15ull * (uint64_t)(lane + 1))) : 0;
+}
+
+// XOR over the wave's 64 lanes; every lane returns the total.
+__device__ __forceinline__ uint64_t wave_xor64(uint64_t h) {
+  int lo = (int)(uint32_t)h, hi = (int)(uint32_t)(h >> 32);
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    lo ^= __shfl_xor(lo, m, kWave);
+    hi ^= __shfl_xor(hi, m, kWave);
+  }
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ uint64_t epoch_salt(uint64_t epoch) { return mix64(epoch ^ 0x5851F42D4C957F2Dull); }
+
+// After a send wave's stores of unit (token, 4 KiB chunk c): the marks of the kBf16VPL 1 KiB
+// chunks it wrote, for each of the token's destination rows (my_row in lanes 0..k-1).
+template <int SYNC>
+__device__ __forceinline__ void publish_marks(const DecomposedArgs& A, const u32x4* buf, const bool* on, int my_row,
+                                              int c, int k, int lane) {
+  uint64_t val[kBf16VPL];
+  if constexpr (SYNC == kDafChecksum) {
+    const uint64_t salt = epoch_salt(A.epoch);
+#pragma unroll
+    for (int u = 0; u < kBf16VPL; ++u) val[u] = wave_xor64(lane_hash(buf[u], on[u], lane)) ^ salt;
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's device-scope row stores are complete
+#pragma unroll
+    for (int u = 0; u < kBf16VPL; ++u) val[u] = A.epoch;
+  }
+  // Index i = j * kBf16VPL + u names destination j's chunk u; lanes take them in rounds of 64.
+  for (int base = 0; base < k * kBf16VPL; base += kWave) {
+    const int i = base + lane;
+    const int j = i / kBf16VPL, u = i % kBf16VPL;
+    const int row = __shfl(my_row, j < k ? j : 0, kWave);
+    uint64_t m = val[0];
+#pragma unroll
+    for (int q = 1; q < kBf16VPL; ++q) m = u == q ? val[q] : m;
+    const int cc = c * kBf16VPL + u;
+    if (j < k && row >= 0 && row < A.cap && cc < A.cchunks) st64_dev(&A.marks[(int64_t)row * A.cchunks + cc], m);
+  }
+}
+
+// Token-Flag Fusion: polls the chunk's mark until it holds the epoch, then loads the lane's vector.
+// The loop condition is wave-uniform (one mark per wave).
+__device__ __forceinline__ bool poll_flag(const uint64_t* mark, uint64_t epoch, const u32x4* row, int nv, int v,
+                                          u32x4& val, int64_t limit) {
+  if (ld64_dev(mark) != epoch) {
+    const int64_t t0 = wall_clock64();
+    do {
+      if (wall_clock64() - t0 > limit) return false;
+      __builtin_amdgcn_s_sleep(1);
+    } while (ld64_dev(mark) != epoch);
+  }
+  val = load_vec_dev(row, nv, v);
+  return true;
+}
+
+// Data-for-Checksum: loads the lane's vector and the chunk's mark until the salted hash of the
+// wave's loaded chunk equals the mark. The comparison is wave-uniform.
+__device__ __forceinline__ bool poll_checksum(const uint64_t* mark, uint64_t salt, const u32x4* row, int nv, int v,
+                                              bool on, int lane, u32x4& val, int64_t limit) {
+  int64_t t0 = -1;
+  while (true) {
+    const uint64_t m = ld64_dev(mark);
+    val = load_vec_dev(row, nv, v);
+    if ((wave_xor64(lane_hash(val, on, lane)) ^ salt) == m) return true;
+    if (t0 < 0)
+      t0 = wall_clock64();
+    else if (wall_clock64() - t0 > limit)
+      return false;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
 // Combine units (token g, 1 KiB column chunk c): one wave per unit, waves iterating on their own.
 // Each wave works out its token's rows as the send role does (no metadata written), then folds
 // the valid rows in j order, acc = fmaf(w_j, y_j, acc) from +0, bf16 round-to-nearest-even, as
 // the combine kernel does.
+template <int SYNC>
 __device__ __forceinline__ void combine_role(const DecomposedArgs& A, int ci, int32_t* lds, int32_t* flag) {
   const Geom& G = A.F.G;
   const int lane = threadIdx.x % kWave;
@@ -253,6 +375,7 @@ __device__ __forceinline__ void combine_role(const DecomposedArgs& A, int ci, in
   const int64_t units = G.T * A.cchunks;
   const int64_t stride = (int64_t)A.nco * kWavesPerBlock;
   const u32x4* y = A.recv;
+  const uint64_t salt = epoch_salt(A.epoch);
   for (int64_t u = (int64_t)ci * kWavesPerBlock + w; u < units; u += stride) {
     const int64_t g = u / A.cchunks;
     const int c = (int)(u - g * A.cchunks);
@@ -271,7 +394,14 @@ __device__ __forceinline__ void combine_role(const DecomposedArgs& A, int ci, in
                                                       __builtin_bit_cast(int, A.topk_w[g * k + j])));
       const u32x4* yr = y + (int64_t)row * A.pv;
       u32x4 val;
-      if (!poll_vec(yr, nv, vl, val, A.spin_ticks)) {
+      bool got;
+      if constexpr (SYNC == kDafFlag)
+        got = poll_flag(A.marks + (int64_t)row * A.cchunks + c, A.epoch, yr, nv, vl, val, A.spin_ticks);
+      else if constexpr (SYNC == kDafChecksum)
+        got = poll_checksum(A.marks + (int64_t)row * A.cchunks + c, salt, yr, nv, vl, on, lane, val, A.spin_ticks);
+      else
+        got = poll_vec(yr, nv, vl, val, A.spin_ticks);
+      if (!got) {
         arrived = false;
         break;
       }
@@ -280,7 +410,7 @@ __device__ __forceinline__ void combine_role(const DecomposedArgs& A, int ci, in
         acc[2 * i] = fmaf(wj, bf16lo_to_f32(val[i]), acc[2 * i]);
         acc[2 * i + 1] = fmaf(wj, bf16hi_to_f32(val[i]), acc[2 * i + 1]);
       }
-      if (on) {  // consumed: back to the sentinel for the next layer
+      if (SYNC == kDafSentinel && on) {  // consumed: back to the sentinel for the next layer
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<u32x4*>(yr), 0, nv * 16,
                                                                            kBufferRsrcWord3);
         const u32x4 s = {kSentinelPair, kSentinelPair, kSentinelPair, kSentinelPair};
@@ -311,7 +441,7 @@ __device__ __forceinline__ void finish(const DecomposedArgs& A) {
   }
 }
 
-template <bool BUF_X, bool LAYER>
+template <bool BUF_X, int SYNC>
 __global__ void __launch_bounds__(kLayoutThreads) decomposed_kernel(DecomposedArgs A) {
   static_assert(kDispatchThreads == kLayoutThreads, "both roles run in 256-thread workgroups");
   extern __shared__ int32_t lds[];
@@ -321,15 +451,32 @@ __global__ void __launch_bounds__(kLayoutThreads) decomposed_kernel(DecomposedAr
   __shared__ int32_t flag;
   if ((int)blockIdx.x < A.nc)
     count_role(A, (int)blockIdx.x, lds, red, scratch, seg_start, &flag);
-  else if (!LAYER || (int)blockIdx.x < A.nc + A.ns)
-    send_role<BUF_X, LAYER>(A, (int)blockIdx.x - A.nc, lds, &flag);
+  else if (SYNC == kDafNone || (int)blockIdx.x < A.nc + A.ns)
+    send_role<BUF_X, SYNC>(A, (int)blockIdx.x - A.nc, lds, &flag);
   else
-    combine_role(A, (int)blockIdx.x - A.nc - A.ns, lds, &flag);
+    combine_role<SYNC>(A, (int)blockIdx.x - A.nc - A.ns, lds, &flag);
   finish(A);
 }
 
 // ------------------------------------------------------------------------ host
 namespace {
+
+template <bool BUF_X>
+void launch_variant(int sync, dim3 grid, dim3 block, size_t lds, hipStream_t stream, const DecomposedArgs& A) {
+  switch (sync) {
+    case kDafSentinel:
+      hipLaunchKernelGGL((decomposed_kernel<BUF_X, kDafSentinel>), grid, block, lds, stream, A);
+      break;
+    case kDafFlag:
+      hipLaunchKernelGGL((decomposed_kernel<BUF_X, kDafFlag>), grid, block, lds, stream, A);
+      break;
+    case kDafChecksum:
+      hipLaunchKernelGGL((decomposed_kernel<BUF_X, kDafChecksum>), grid, block, lds, stream, A);
+      break;
+    default:
+      hipLaunchKernelGGL((decomposed_kernel<BUF_X, kDafNone>), grid, block, lds, stream, A);
+  }
+}
 
 size_t decomposed_lds_bytes(const Geom& g) {
   const size_t hist = (size_t)g.E + g.R + kMaxChunkPairs;                       // K1
@@ -340,20 +487,30 @@ size_t decomposed_lds_bytes(const Geom& g) {
 
 }  // namespace
 
-template <bool BUF_X, bool LAYER>
+template <bool BUF_X, int SYNC>
 static hipError_t occupancy(int* per_cu, size_t lds) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, decomposed_kernel<BUF_X, LAYER>, kLayoutThreads, lds);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, decomposed_kernel<BUF_X, SYNC>, kLayoutThreads, lds);
 }
 
-hipError_t plan_decomposed(const Geom& g, int H, int count_groups, bool layer, DecomposedPlan* plan) {
+template <bool BUF_X>
+static hipError_t occupancy_of(int sync, int* per_cu, size_t lds) {
+  switch (sync) {
+    case kDafSentinel: return occupancy<BUF_X, kDafSentinel>(per_cu, lds);
+    case kDafFlag: return occupancy<BUF_X, kDafFlag>(per_cu, lds);
+    case kDafChecksum: return occupancy<BUF_X, kDafChecksum>(per_cu, lds);
+    default: return occupancy<BUF_X, kDafNone>(per_cu, lds);
+  }
+}
+
+hipError_t plan_decomposed(const Geom& g, int H, int count_groups, int sync, DecomposedPlan* plan) {
+  const bool layer = sync != kDafNone;
   int dev = 0, cus = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   const bool buf_x = g.T * (int64_t)H * 2 >= kBufferLoadXBytes;
   const size_t lds = decomposed_lds_bytes(g);
   if (e == hipSuccess)
-    e = layer ? (buf_x ? occupancy<true, true>(&per_cu, lds) : occupancy<false, true>(&per_cu, lds))
-              : (buf_x ? occupancy<true, false>(&per_cu, lds) : occupancy<false, false>(&per_cu, lds));
+    e = buf_x ? occupancy_of<true>(sync, &per_cu, lds) : occupancy_of<false>(sync, &per_cu, lds);
   if (e != hipSuccess) return e;
   plan->capacity = per_cu * cus;
   // Default split: one count workgroup per layout chunk, at most a quarter of what the device
@@ -380,10 +537,10 @@ hipError_t plan_decomposed(const Geom& g, int H, int count_groups, bool layer, D
 
 hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, const epl_layout_buffers& L,
                              const void* x, void* recv, int H, int pitch, int64_t cap, const DecomposedOpts& opts,
-                             int32_t* wait_status, hipStream_t stream, const float* topk_w, void* out) {
-  const bool layer = out != nullptr;
+                             int32_t* wait_status, hipStream_t stream, int sync, const float* topk_w, void* out,
+                             uint64_t* marks, uint64_t epoch) {
   DecomposedPlan plan;
-  hipError_t e = plan_decomposed(g, H, opts.count_groups, layer, &plan);
+  hipError_t e = plan_decomposed(g, H, opts.count_groups, sync, &plan);
   if (e != hipSuccess) return e;
   if (plan.grid > plan.capacity) return hipErrorLaunchOutOfResources;  // refused on the host before this
   const WsLayout wl = ws_layout(g);
@@ -405,6 +562,8 @@ hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, con
   A.cnt = ws + wl.cnt;
   A.topk_w = topk_w;
   A.out = static_cast<u32x4*>(out);
+  A.marks = marks;
+  A.epoch = epoch;
   A.x = static_cast<const u32x4*>(x);
   A.recv = static_cast<u32x4*>(recv);
   A.nv = H / 8;
@@ -422,17 +581,10 @@ hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, con
   const size_t lds = decomposed_lds_bytes(g);
   const bool buf_x = g.T * (int64_t)H * 2 >= kBufferLoadXBytes;
   const dim3 grid(plan.grid), block(kLayoutThreads);
-  if (layer) {
-    if (buf_x)
-      hipLaunchKernelGGL((decomposed_kernel<true, true>), grid, block, lds, stream, A);
-    else
-      hipLaunchKernelGGL((decomposed_kernel<false, true>), grid, block, lds, stream, A);
-  } else {
-    if (buf_x)
-      hipLaunchKernelGGL((decomposed_kernel<true, false>), grid, block, lds, stream, A);
-    else
-      hipLaunchKernelGGL((decomposed_kernel<false, false>), grid, block, lds, stream, A);
-  }
+  if (buf_x)
+    launch_variant<true>(sync, grid, block, lds, stream, A);
+  else
+    launch_variant<false>(sync, grid, block, lds, stream, A);
   return hipGetLastError();
 }
 

@@ -290,14 +290,20 @@ struct DecomposedOpts {
 struct DecomposedPlan {
   int grid, count_groups, send_groups, combine_groups, capacity;
 };
-// layer: the variant with combine workgroups (Sentinel Polling).
-hipError_t plan_decomposed(const Geom& g, int H, int count_groups, bool layer, DecomposedPlan* plan);
-// With out != nullptr, the layer variant: combine workgroups gather the rows into out with the
-// weights topk_w as the send workgroups write them.
+// How the layer variants' combine workgroups learn that a row chunk has arrived (Data-as-Flag):
+// kDafNone is the launch without combine workgroups (layout and dispatch only).
+constexpr int kDafNone = 0;       // no combine role
+constexpr int kDafSentinel = 1;   // Sentinel Polling: every element compared with the reserved pattern
+constexpr int kDafFlag = 2;       // Token-Flag Fusion: an epoch flag per 1 KiB chunk, stored after the chunk
+constexpr int kDafChecksum = 3;   // Data-for-Checksum: a salted hash per 1 KiB chunk, checked against the data
+hipError_t plan_decomposed(const Geom& g, int H, int count_groups, int sync, DecomposedPlan* plan);
+// sync != kDafNone: the layer variant, whose combine workgroups gather the rows into out with the
+// weights topk_w as the send workgroups write them; marks and epoch serve kDafFlag and kDafChecksum.
 hipError_t launch_decomposed(const Geom& g, const int32_t* idx, int32_t* ws, const epl_layout_buffers& L,
                              const void* x, void* recv, int H, int pitch, int64_t cap, const DecomposedOpts& opts,
-                             int32_t* wait_status, hipStream_t stream, const float* topk_w = nullptr,
-                             void* out = nullptr);
+                             int32_t* wait_status, hipStream_t stream, int sync = kDafNone,
+                             const float* topk_w = nullptr, void* out = nullptr, uint64_t* marks = nullptr,
+                             uint64_t epoch = 0);
 // Every 16-byte vector of buf [nvec] set to the bf16 sentinel.
 hipError_t launch_sentinel_fill(void* buf, int64_t nvec, hipStream_t stream);
 // y rows are pitch elements apart.

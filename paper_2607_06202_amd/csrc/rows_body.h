@@ -52,14 +52,19 @@ __device__ __forceinline__ void store_row_policy(u32x4 val, u32x4* row_base, int
 // row_of() returns, in lane j < k, the packed row of pair j (-1 if invalid); it is called after the
 // loads of x are issued, so whatever it loads is in flight together with them. An inactive wave
 // loads and calls row_of() (which may hold a workgroup barrier) but stores nothing. check(buf, on)
-// sees the unit's loaded vectors (on[u]: vector u lies inside the row) before they are stored.
+// sees the unit's loaded vectors (on[u]: vector u lies inside the row) before they are stored, and
+// after(buf, on, my_row) runs once they are issued (my_row: lane j's packed row, as above).
 struct NoCheck {
   __device__ __forceinline__ void operator()(const u32x4*, const bool*) const {}
 };
-template <bool BUF_X, class RowFn, class CheckFn = NoCheck>
+struct NoAfter {
+  __device__ __forceinline__ void operator()(const u32x4*, const bool*, int) const {}
+};
+template <bool BUF_X, class RowFn, class CheckFn = NoCheck, class AfterFn = NoAfter>
 __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, RowFn row_of, u32x4* __restrict__ recv,
                                                    int64_t g, int c, int k, int nv, int pv, int64_t cap, int lane,
-                                                   bool active = true, CheckFn check = CheckFn()) {
+                                                   bool active = true, CheckFn check = CheckFn(),
+                                                   AfterFn after = AfterFn()) {
   const u32x4* xr = x + g * nv;
   const int v0 = c * kBf16Cols + lane;
   // Loads are unconditional (index clamped into the row) so that all of them are in flight
@@ -89,6 +94,7 @@ __device__ __forceinline__ void dispatch_bf16_unit(const u32x4* __restrict__ x, 
       if (v < nv) store_row_policy<kCachePolicySc1>(buf[u], recv + (int64_t)row * pv, nv, v);
     }
   }
+  after(buf, on, my_row);
 }
 
 // fp8: unit = (token g, pass p) covering elements [1024p, 1024p + 1024). Lane l quantises

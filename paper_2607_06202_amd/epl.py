@@ -90,6 +90,8 @@ WAIT_GAVE_UP_SEND = 2     # EPL_WAIT_GAVE_UP_SEND
 WAIT_GAVE_UP_COMBINE = 4  # EPL_WAIT_GAVE_UP_COMBINE
 WAIT_SENTINEL_IN_X = 8    # EPL_WAIT_SENTINEL_IN_X
 SENTINEL_BF16 = 0xFFFF    # EPL_SENTINEL_BF16
+DAF_TOKEN_FLAG_FUSION = 1  # EPL_DAF_TOKEN_FLAG_FUSION
+DAF_DATA_CHECKSUM = 2      # EPL_DAF_DATA_CHECKSUM
 
 
 class LayoutBuffers(ctypes.Structure):
@@ -145,6 +147,11 @@ def lib() -> ctypes.CDLL:
                                           ctypes.POINTER(ctypes.c_int32)]
         L.epl_layer_sentinel.restype = ctypes.c_int
         L.epl_layer_sentinel.argtypes = [CP, P, LP, P, S, P, P, I64, P, P, ctypes.POINTER(DecomposedOpts), P, P]
+        L.epl_layer_data_as_flag.restype = ctypes.c_int
+        L.epl_layer_data_as_flag.argtypes = [CP, P, LP, P, S, P, P, I64, P, P, P, ctypes.c_int32, ctypes.c_uint64,
+                                             ctypes.POINTER(DecomposedOpts), P, P]
+        L.epl_layer_marks_bytes.restype = I64
+        L.epl_layer_marks_bytes.argtypes = [CP, I64]
         L.epl_sentinel_fill.restype = ctypes.c_int
         L.epl_sentinel_fill.argtypes = [P, I64, P]
         L.epl_sentinel_find.restype = I64
@@ -542,6 +549,62 @@ def layer_sentinel(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, topk_w:
                                         L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
                                         rows, topk_w.data_ptr(), out.data_ptr(), ctypes.byref(opts), status.data_ptr(),
                                         _stream(dev)), "epl_layer_sentinel")
+    return L, out, status
+
+
+def layer_marks_bytes(cfg: Config, rows: int | None = None) -> int:
+    """epl_layer_marks_bytes: bytes of the marks buffer of layer_data_as_flag for `rows` receive
+    rows (T*k by default)."""
+    n = int(lib().epl_layer_marks_bytes(ctypes.byref(cfg), recv_rows_cap(cfg) if rows is None else rows))
+    if n < 0:
+        raise EplError(1, "epl_layer_marks_bytes(%r)" % (cfg,))
+    return n
+
+
+def alloc_marks(cfg: Config, device, rows: int | None = None) -> torch.Tensor:
+    """A zero-filled marks buffer for layer_data_as_flag: one int64 word per (receive row, 1 KiB
+    column chunk)."""
+    n = layer_marks_bytes(cfg, rows) // 8
+    return torch.zeros(max(n, 1), dtype=torch.int64, device=device)
+
+
+def layer_data_as_flag(cfg: Config, topk_idx: torch.Tensor, x: torch.Tensor, topk_w: torch.Tensor,
+                       recv: torch.Tensor, marks: torch.Tensor, variant: int, epoch: int,
+                       out: torch.Tensor | None = None, layout_out: Layout | None = None, count_groups: int = 0,
+                       spin_limit_us: int = 0, test_ready_target: int = 0, status: torch.Tensor | None = None):
+    """epl_layer_data_as_flag: the one-launch layer with the combine synchronised per 1 KiB chunk by
+    Token-Flag Fusion (variant DAF_TOKEN_FLAG_FUSION) or Data-for-Checksum (DAF_DATA_CHECKSUM).
+    marks: from alloc_marks (zero-filled), kept from call to call; epoch: nonzero, a new value on
+    every call (for Token-Flag Fusion, never one used before on these marks). -> (Layout,
+    out [T, H] bf16, status [1] int32)."""
+    dev = topk_idx.device
+    if cfg.payload != PAYLOAD_BF16:
+        raise EplError(5, "epl_layer_data_as_flag (bf16 only)")
+    L = _layout_args(cfg, topk_idx, layout_out)
+    recv, _, _, rows = _recv_args(cfg, x, recv, None, dev)
+    _dev(marks, "marks", torch.int64)
+    if marks.numel() * 8 < layer_marks_bytes(cfg, rows):
+        raise ValueError("marks has %d bytes, needs %d" % (marks.numel() * 8, layer_marks_bytes(cfg, rows)))
+    _dev(topk_w, "topk_w", torch.float32)
+    if _rows_of(topk_w, "topk_w", cfg.topk) < cfg.T:
+        raise ValueError("topk_w has %d rows, needs T = %d" % (topk_w.shape[0], cfg.T))
+    if out is None:
+        out = torch.empty(max(cfg.T, 1), cfg.hidden, dtype=torch.bfloat16, device=dev)
+    _dev(out, "out", torch.bfloat16)
+    if _rows_of(out, "out", cfg.hidden) < cfg.T:
+        raise ValueError("out has %d rows, needs T = %d" % (out.shape[0], cfg.T))
+    if status is None:
+        status = torch.empty(1, dtype=torch.int32, device=dev)
+    _dev(status, "status", torch.int32)
+    _same_device(dev, topk_w=topk_w, out=out, status=status, marks=marks)
+    opts = DecomposedOpts(count_groups, spin_limit_us, test_ready_target)
+    bufs = L.buffers()
+    with _on(dev):
+        _check(lib().epl_layer_data_as_flag(ctypes.byref(cfg), topk_idx.data_ptr(), ctypes.byref(bufs),
+                                            L.workspace.data_ptr(), L.workspace.numel(), x.data_ptr(), recv.data_ptr(),
+                                            rows, topk_w.data_ptr(), out.data_ptr(), marks.data_ptr(), variant, epoch,
+                                            ctypes.byref(opts), status.data_ptr(), _stream(dev)),
+               "epl_layer_data_as_flag")
     return L, out, status
 
 

@@ -348,6 +348,37 @@ def test_layer_sentinel_errors_before_any_hip_call(lib):
     assert lib.epl_sentinel_fill(Fake.ptr(1, 8), 16, None) == ALIGN
 
 
+def test_layer_data_as_flag_errors_before_any_hip_call(lib):
+    """The flag and checksum layer: every argument error is reported before the call touches the
+    GPU (the calls below use fake pointers and would fault if they launched)."""
+    L = fake_layout()
+    c = epl.config(4, 16, 2, 256, 128)
+    idx, ws, x, recv, w, out, st, marks = (Fake.ptr(i) for i in (50, 60, 70, 71, 80, 81, 90, 91))
+
+    def f(c=c, w=w, out=out, st=st, marks=marks, variant=epl.DAF_DATA_CHECKSUM, epoch=1, opts=None):
+        return lib.epl_layer_data_as_flag(ctypes.byref(c), idx, ctypes.byref(L), ws, 1 << 30, x, recv, 4 * 128 * 2, w,
+                                          out, marks, variant, epoch, ctypes.byref(opts) if opts is not None else None,
+                                          st, None)
+    for variant in (epl.DAF_TOKEN_FLAG_FUSION, epl.DAF_DATA_CHECKSUM):
+        assert f(variant=variant, marks=None) == INVALID
+        assert f(variant=variant, marks=Fake.ptr(91, 4)) == ALIGN
+        assert f(variant=variant, epoch=0) == INVALID
+        assert f(variant=variant, w=None) == INVALID
+        assert f(variant=variant, out=Fake.ptr(81, 8)) == ALIGN
+        assert f(variant=variant, st=None) == INVALID
+        assert f(variant=variant, opts=epl.DecomposedOpts(-1, 0, 0)) == INVALID
+        assert f(variant=variant, c=epl.config(4, 16, 2, 256, 128, "fp8")) == INVALID  # no scale buffer
+        assert f(variant=variant, c=epl.config(4, 16, 2, 256, 128, row_pitch=300)) == INVALID
+    for variant in (0, 3, -1):
+        assert f(variant=variant) == INVALID
+    assert f(variant=0, c=epl.config(4, 15, 2, 256, 128)) == INVALID  # the config is checked first
+    assert lib.epl_layer_marks_bytes(ctypes.byref(c), 1024) == 1024 * 1 * 8  # H = 256: one 1 KiB chunk
+    assert lib.epl_layer_marks_bytes(ctypes.byref(epl.config(64, 256, 8, 7168, 128)), 65536) == 65536 * 14 * 8
+    assert lib.epl_layer_marks_bytes(ctypes.byref(epl.config(2, 4, 1, 520, 3)), 7) == 7 * 2 * 8  # a ragged chunk
+    assert lib.epl_layer_marks_bytes(ctypes.byref(c), -1) == -1
+    assert lib.epl_layer_marks_bytes(ctypes.byref(epl.config(4, 15, 2, 256, 128)), 8) == -1
+
+
 def test_schedule_errors_before_any_hip_call(lib):
     """epl_hop_schedule and epl_dispatch_scheduled report bad worker counts, class counts, remap
     rows, payloads, missing buffers, misalignment and capacity before they touch the HIP runtime."""
