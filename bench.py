@@ -448,6 +448,9 @@ def main():
     ap.add_argument("--sentinel-layer", action="store_true",
                     help="time epl_layer_sentinel: layout, dispatch and the combine of the dispatched rows in one "
                          "launch, synchronised per row by Sentinel Polling")
+    ap.add_argument("--layer-flags", choices=["flag", "checksum"], default=None,
+                    help="time epl_layer_data_as_flag: the one-launch layer synchronised per 1 KiB chunk by "
+                         "Token-Flag Fusion (flag) or Data-for-Checksum (checksum), a new epoch every call")
     ap.add_argument("--scheduled", type=int, default=0, metavar="WORKERS",
                     help="time epl_layout + epl_dispatch_scheduled (WORKERS workgroups per source rank, each "
                          "sending one equal slice of the rank's pairs in the transposed expert order) + epl_combine")
@@ -560,12 +563,21 @@ def main():
     else:
         y = recv
 
-    mode = ("sentinel" if args.sentinel_layer else "decomposed" if args.decomposed else
+    mode = ("sentinel" if args.sentinel_layer else args.layer_flags if args.layer_flags else
+            "decomposed" if args.decomposed else
             "scheduled" if args.scheduled else "fused" if args.fused else "separate")
+    layer_modes = ("sentinel", "flag", "checksum")  # one launch for the whole layer, combine included
+    if mode in layer_modes and w.payload != "bf16":
+        raise SystemExit("the one-launch layers run bf16 layers only")
     if mode == "sentinel":
-        if w.payload != "bf16":
-            raise SystemExit("--sentinel-layer runs bf16 layers only")
         epl.sentinel_fill(recv)  # once; every layer leaves the receive buffer so
+    marks = None
+    epoch = [0]
+    if mode in ("flag", "checksum"):
+        if args.graph:
+            raise SystemExit("--layer-flags takes a new epoch on every call, which a graph replay cannot")
+        marks = epl.alloc_marks(cfg, dev, recv.shape[0])
+        variant = epl.DAF_TOKEN_FLAG_FUSION if mode == "flag" else epl.DAF_DATA_CHECKSUM
     status_d = torch.zeros(1, dtype=torch.int32, device=dev)
 
     def layout_dispatch(i, mark=None):
@@ -577,6 +589,12 @@ def main():
                 mark()
             epl.layer_sentinel(cfg, idx_d, xi, w_d, recv, out=out, layout_out=L, count_groups=args.count_groups,
                                status=status_d)
+        elif mode in ("flag", "checksum"):  # likewise, with a new epoch each call
+            if mark is not None:
+                mark()
+            epoch[0] += 1
+            epl.layer_data_as_flag(cfg, idx_d, xi, w_d, recv, marks, variant, epoch[0], out=out, layout_out=L,
+                                   count_groups=args.count_groups, status=status_d)
         elif mode == "decomposed":
             if mark is not None:
                 mark()
@@ -610,7 +628,7 @@ def main():
         layout_dispatch(i, None if ev is None else (lambda: ev[1].record(stream)))
         if ev is not None:
             ev[2].record(stream)
-        if mode != "sentinel":
+        if mode not in layer_modes:
             epl.combine(cfg, y, w_d, L, out)
         if ev is not None:
             ev[3].record(stream)
@@ -691,7 +709,7 @@ def main():
                 layout_dispatch(i)
                 if ev is not None:
                     ev[0].record(stream)
-            if mode != "sentinel":
+            if mode not in layer_modes:
                 epl.combine(cfg, y, w_d, L, out)
             if ev is not None and dom == "combine":
                 ev[1].record(stream)
@@ -723,8 +741,8 @@ def main():
     dev_ev = {**in_region, **top_up}
 
     decomposed_split = None
-    if mode == "sentinel" and int(status_d.item()) != 0:
-        raise RuntimeError("a wait of the Sentinel Polling layer gave up (status %d)" % int(status_d.item()))
+    if mode in layer_modes and int(status_d.item()) != 0:
+        raise RuntimeError("a wait of the one-launch layer gave up (status %d)" % int(status_d.item()))
     if mode == "decomposed":
         if int(status_d.item()) != 0:
             raise RuntimeError("a wait of the decomposed launch gave up (status %d)" % int(status_d.item()))
@@ -747,6 +765,7 @@ def main():
     pct = lambda a: [round(float(v), 2) for v in np.percentile(a, [10, 50, 90])]
     legs = {"decomposed": ("before_launch", "layout_dispatch_decomposed"), "fused": ("layout_counts", "dispatch_rows"),
             "separate": ("layout", "dispatch"), "sentinel": ("before_launch", "layer_sentinel"),
+            "flag": ("before_launch", "layer_data_as_flag"), "checksum": ("before_launch", "layer_data_as_flag"),
             "scheduled": ("layout", "dispatch_scheduled")}[mode]
     percentiles = {legs[0]: pct(per[:, 0]), legs[1]: pct(per[:, 1]), "combine": pct(per[:, 2]),
                    "layer": pct(per.sum(axis=1))}
@@ -761,16 +780,16 @@ def main():
 
     # The dispatch leg is one kernel: the plain dispatch kernel, or (epl_dispatch_rows with the
     # layout's finalize fused in) the fused row kernel, whose bytes include the placement metadata.
-    launches = 1 if mode in ("decomposed", "sentinel") else epl.layout_dispatch_launches(cfg) if mode == "fused" else None
+    launches = 1 if mode in ("decomposed",) + layer_modes else epl.layout_dispatch_launches(cfg) if mode == "fused" else None
     row_fused = mode == "fused" and launches == 3
     if mode == "decomposed" and dom == "dispatch":
         dom_bytes = nbytes["layout"] + nbytes["dispatch"]  # the one launch does the whole layout and dispatch
-    elif mode == "sentinel":
+    elif mode in layer_modes:
         dom, dom_bytes = "dispatch", nbytes["total"]  # the one launch is the whole layer
     else:
         dom_bytes = nbytes["rows_fused" if row_fused and dom == "dispatch" else dom]
     achieved = dom_bytes / (dom_us * 1e-6) / 1e9
-    kname = {"dispatch": "decomposed_kernel" if mode in ("decomposed", "sentinel") else
+    kname = {"dispatch": "decomposed_kernel" if mode in ("decomposed",) + layer_modes else
              "dispatch_scheduled_kernel" if mode == "scheduled" else
              "fused_bf16_kernel" if row_fused else
              "dispatch_fp8_kernel" if w.payload == "fp8" else "dispatch_bf16_kernel",
@@ -815,6 +834,8 @@ def main():
         "device": device_end(dinfo),
         "launch": "graph" if graphs is not None else "eager",
         "calls": {"decomposed": "epl_layout_dispatch_decomposed + epl_combine", "sentinel": "epl_layer_sentinel",
+                  "flag": "epl_layer_data_as_flag (Token-Flag Fusion)",
+                  "checksum": "epl_layer_data_as_flag (Data-for-Checksum)",
                   "fused": "epl_layout_dispatch + epl_combine",
                   "separate": "epl_layout + epl_dispatch + epl_combine",
                   "scheduled": "epl_layout + epl_dispatch_scheduled + epl_combine"}[mode],
