@@ -1,6 +1,7 @@
 // Standalone C++ consumer of the C ABI in include/epl.h: no Python, no torch. It allocates
 // device buffers with the HIP runtime, runs layout -> dispatch -> combine, the row location, the
-// hierarchical schedule and the dispatch in its order on its own stream, and compares every output
+// hierarchical schedule and the dispatch in its order, and the one-launch layer synchronised by
+// Token-Flag Fusion and by Data-for-Checksum on its own stream, and compares every output
 // with the CPU oracle (oracle/liboracle.so, test
 // infrastructure), then checks that host-detectable errors are reported before anything is launched.
 // Prints "c abi check ok" and exits 0 on success; prints the first difference and exits 1.
@@ -277,6 +278,83 @@ bool run_case(const Case& c, uint64_t seed, hipStream_t stream, Mode mode) {
   return ok;
 }
 
+// The one-launch layer synchronised by Token-Flag Fusion or Data-for-Checksum: two consecutive
+// calls (epochs 1 and 2) on one marks buffer, each output against the oracle's combine of x's rows.
+bool run_layer_case(int variant, uint64_t seed, hipStream_t stream) {
+  const int R = 8, E = 32, k = 4, Tr = 50, H = 1024;
+  const int64_t T = (int64_t)R * Tr, Tk = T * k;
+  epl_config cfg{R, E, k, H, Tr, EPL_PAYLOAD_BF16, 0};
+  std::vector<int32_t> idx(Tk);
+  for (auto& v : idx) v = (int32_t)(splitmix(seed) % (uint64_t)(E + 2)) - 1;
+  std::vector<uint16_t> x((size_t)T * H);
+  for (auto& v : x) v = (uint16_t)(0x3C00 + (splitmix(seed) % 0x0800) - 0x0400);
+  std::vector<float> w(Tk);
+  for (auto& v : w) v = (float)(splitmix(seed) % 1000) / 1000.0f;
+  std::vector<int32_t> r_send(R * E), r_rank(R * R), r_eoff(E + 1), r_roff(R + 1), r_seg(E * R), r_ntok(T), r_row(Tk),
+      r_slot(Tk), r_src(Tk), r_j(Tk), r_inv(1);
+  eplref_layout(R, E, k, Tr, idx.data(), r_send.data(), r_rank.data(), r_eoff.data(), r_roff.data(), r_seg.data(),
+                r_ntok.data(), r_row.data(), r_slot.data(), r_src.data(), r_j.data(), r_inv.data());
+  const int32_t P = r_eoff[E];
+  std::vector<uint16_t> y((size_t)std::max<int32_t>(P, 1) * H);
+  for (int32_t r = 0; r < P; ++r) std::memcpy(&y[(size_t)r * H], &x[(size_t)r_src[r] * H], H * 2);
+  std::vector<uint16_t> want((size_t)T * H);
+  eplref_combine(T, k, H, y.data(), w.data(), r_row.data(), nullptr, T, want.data());
+
+  int32_t* d_idx = dev_copy(idx);
+  const size_t sizes[] = {(size_t)R * E, (size_t)R * R, (size_t)E + 1, (size_t)R + 1, (size_t)E * R, (size_t)T,
+                          (size_t)Tk,    (size_t)Tk,    (size_t)Tk,    (size_t)Tk,    1};
+  std::vector<int32_t*> d_out;
+  for (size_t n : sizes) {
+    int32_t* q = nullptr;
+    HIP_OK(hipMalloc(&q, n * 4));
+    d_out.push_back(q);
+  }
+  epl_layout_buffers L{d_out[0], d_out[1], d_out[2], d_out[3], d_out[4], d_out[5],
+                       d_out[6], d_out[7], d_out[8], d_out[9], d_out[10]};
+  const size_t ws_bytes = epl_workspace_bytes(&cfg);
+  void* ws = nullptr;
+  HIP_OK(hipMalloc(&ws, ws_bytes));
+  HIP_OK(hipMemset(ws, 0, ws_bytes));  // the one-launch calls' synchronisation words start at zero
+  uint16_t* d_x = dev_copy(x);
+  float* d_w = dev_copy(w);
+  void *d_recv = nullptr, *d_o = nullptr, *d_marks = nullptr;
+  int32_t* d_status = nullptr;
+  HIP_OK(hipMalloc(&d_recv, (size_t)Tk * H * 2));
+  HIP_OK(hipMalloc(&d_o, (size_t)T * H * 2));
+  const int64_t marks_bytes = epl_layer_marks_bytes(&cfg, Tk);
+  HIP_OK(hipMalloc(&d_marks, marks_bytes));
+  HIP_OK(hipMemset(d_marks, 0, marks_bytes));
+  HIP_OK(hipMalloc(&d_status, 4));
+  bool ok = marks_bytes == Tk * 2 * 8;
+  for (uint64_t epoch = 1; ok && epoch <= 2; ++epoch) {
+    ok = epl_layer_data_as_flag(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, Tk, d_w, d_o, (uint64_t*)d_marks,
+                                variant, epoch, nullptr, d_status, stream) == EPL_OK;
+    HIP_OK(hipStreamSynchronize(stream));
+    ok = ok && host_copy(d_status, 1)[0] == 0 && same("layer pair_row", host_copy(d_out[6], Tk), r_row, Tk) &&
+         same("layer combine", host_copy((const uint16_t*)d_o, (size_t)T * H), want, (size_t)T * H);
+  }
+  ok = ok &&
+       epl_layer_data_as_flag(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, Tk, d_w, d_o, (uint64_t*)d_marks, variant,
+                              0, nullptr, d_status, stream) == EPL_ERR_INVALID_ARG &&
+       epl_layer_data_as_flag(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, Tk, d_w, d_o, (uint64_t*)d_marks, 7, 3,
+                              nullptr, d_status, stream) == EPL_ERR_INVALID_ARG &&
+       epl_layer_data_as_flag(&cfg, d_idx, &L, ws, ws_bytes, d_x, d_recv, Tk, d_w, d_o,
+                              (uint64_t*)((char*)d_marks + 4), variant, 3, nullptr, d_status,
+                              stream) == EPL_ERR_ALIGN;
+  for (int32_t* q : d_out) HIP_OK(hipFree(q));
+  HIP_OK(hipFree(d_idx));
+  HIP_OK(hipFree(ws));
+  HIP_OK(hipFree(d_x));
+  HIP_OK(hipFree(d_w));
+  HIP_OK(hipFree(d_recv));
+  HIP_OK(hipFree(d_o));
+  HIP_OK(hipFree(d_marks));
+  HIP_OK(hipFree(d_status));
+  std::printf("layer R=%d E=%d k=%d Tr=%d H=%d %s, epochs 1 and 2: %s\n", R, E, k, Tr, H,
+              variant == EPL_DAF_TOKEN_FLAG_FUSION ? "Token-Flag Fusion" : "Data-for-Checksum", ok ? "ok" : "FAILED");
+  return ok;
+}
+
 }  // namespace
 
 int main() {
@@ -299,6 +377,7 @@ int main() {
     for (Mode m : {kSeparate, kOneCall, kTwoPhases}) ok = run_case(c, seed, stream, m) && ok;
     ++seed;
   }
+  for (int variant : {EPL_DAF_TOKEN_FLAG_FUSION, EPL_DAF_DATA_CHECKSUM}) ok = run_layer_case(variant, seed++, stream) && ok;
   HIP_OK(hipStreamDestroy(stream));
   if (!ok) return 1;
   std::printf("c abi check ok\n");

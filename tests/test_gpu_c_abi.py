@@ -1,8 +1,9 @@
 """The C ABI used from C++ with no Python in the process: tests/c_abi/epl_c_check allocates its own
 device buffers, runs layout -> dispatch -> combine through include/epl.h on its own HIP stream (as
 epl_layout + epl_dispatch, as one epl_layout_dispatch call and as its two phases), with packed rows
-and with rows a pitch apart, compares every output with the CPU oracle, and checks the documented
-error statuses."""
+and with rows a pitch apart, plus the one-launch layer synchronised by Token-Flag Fusion and by
+Data-for-Checksum, compares every output with the CPU oracle, and checks the documented error
+statuses."""
 import os
 import subprocess
 
@@ -20,4 +21,4 @@ def test_c_abi_standalone_program():
     print(r.stdout)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "c abi check ok" in r.stdout
-    assert r.stdout.count(": ok") == 24  # 8 cases x 3 ways of calling
+    assert r.stdout.count(": ok") == 26  # 8 cases x 3 ways of calling, and the two layer variants
