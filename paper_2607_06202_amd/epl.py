@@ -65,11 +65,12 @@ def config(R: int, E: int, k: int, H: int, Tr: int, payload: str | int = "bf16",
 # Row pitches measured faster than packed rows on MI355X, by (H, payload); other shapes keep packed
 # rows. Whole layer, one box, 200 steps per pitch (us per layer):
 # * H = 7168 bf16, EP=64 decode: 7168 376.7-377.3, 7424 377.1, 7680 375.1, 7936 373.8, 8192 392.0,
-#   8448 374.5, 9216 381.4 (on other boxes 7936 gained 0.6-3.6%); EP=256, prefill and the DeepSeek
-#   shape neutral (within 0.3%);
+#   8448 374.5, 9216 381.4 (on other boxes 7936 gained 0.6-3.6%); prefill and the DeepSeek shape
+#   within 0.3% of packed rows; EP=256 0.2% faster at 7936 and 1.1% faster at 7680, which costs prefill
+#   0.3% (one pitch per row size is kept);
 # * H = 5120 bf16 (GLM-4.7 shape): 5120 131.8-132.2, 5248 131.6, 5632 134.5, 5888 144.5, 8192 141.9;
 # * H = 2048 bf16 (Qwen3-30B shape): 39.5-40.1 at every pitch (bound by launches);
-# * H = 7168 fp8: a pitch of 7936 bytes 0.3-0.7% slower.
+# * H = 7168 fp8: packed 556.0-556.3, every pitch from 7232 to 9216 bytes 556.5-563.2.
 TUNED_PITCH = {(7168, PAYLOAD_BF16): 7936}
 
 
